@@ -1,0 +1,167 @@
+/*
+ * sol_attn.h -- C ABI of the MI355X (gfx950) routed-attention library
+ * (Sol-Attn forward pass: threshold routing, exact block-sparse attention and
+ * proxy-score reuse fused into one online-softmax pass).
+ *
+ * All tensors are caller-owned, contiguous, row-major device buffers of shape
+ * [B, H, N, d] (row stride d) unless stated otherwise.  Every entry point
+ * validates its arguments on the host and returns a negative error code before
+ * any GPU call when they are invalid; sol_attn_last_error() then describes the
+ * problem.  Compute calls are asynchronous on the given HIP stream (a
+ * hipStream_t passed as void*; NULL means the default stream) and do not
+ * synchronise it.  GPU faults surface as SOL_ERR_HIP from a later synchronising
+ * call (sol_attn_stats).
+ *
+ * Supported shapes: d in {64, 128}; block_k = 64; block_q in {64, 128};
+ * N >= 1 with ragged last blocks (a block's statistics use only its valid
+ * tokens); bf16 inputs (the hot path) and f32 inputs (a correctness-first
+ * path).  The softmax scale is 1/sqrt(d) for the exact logits and the
+ * proxies alike.  bf16 value inputs must lie within the f16 range
+ * (|v| <= 65504): the value operand of the probability-times-value products
+ * is carried in f16.
+ */
+#ifndef SOL_ATTN_H
+#define SOL_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Forward modes. */
+enum {
+    SOL_DENSE = 0,                /* softmax(QK^T/sqrt(d))V over all keys (Section 2, Eq. dense_attn) */
+    SOL_SPARSE = 1,               /* routed exact blocks + zeroth-order correction
+                                     (Section 3.2, Eqs. solattn_denominator and solattn_numerator) */
+    SOL_SPARSE_NO_CORRECTION = 2  /* routed exact blocks only (Section 2, Eq. block_sparse_attn) */
+};
+
+/* Element types of q, k, v and out. */
+enum { SOL_BF16 = 0, SOL_F32 = 1 };
+
+/* Return codes. */
+enum {
+    SOL_OK = 0,
+    SOL_ERR_INVALID_ARG = -1,  /* null pointer, non-positive size, bad mode/dtype, NaN cutoff */
+    SOL_ERR_UNSUPPORTED = -2,  /* valid but unsupported shape (d, block sizes, too many blocks) */
+    SOL_ERR_HIP = -3,          /* a HIP runtime call failed (allocation, launch, sync) */
+    SOL_ERR_WORKSPACE = -4,    /* caller workspace smaller than sol_attn_workspace_bytes() */
+    SOL_ERR_NO_DATA = -5       /* sol_attn_stats before any forward, or B/H mismatch */
+};
+
+/*
+ * Block mean pooling (Section 2, Eq. block_proxy: Qbar_i = Mean(Q_i),
+ * Kbar_j = Mean(K_j); and the pooled values behind V_hat_j of Eq.
+ * solattn_numerator, here as the mean, V_hat_j = n_j * Vbar_j).
+ *
+ * q, k, v:   [B,H,N,d] device, element type `dtype`.  A pointer may be NULL
+ *            when the matching output is NULL.
+ * qbar:      [B,H,ceil(N/block_q),d] f32 device, or NULL to skip.
+ * kbar,vbar: [B,H,ceil(N/block_k),d] f32 device, or NULL to skip.
+ * The last block of each kind averages only its n = N - (nb-1)*block valid
+ * tokens.  Accumulation is in f32.
+ */
+int sol_attn_pool_blocks(const void* q, const void* k, const void* v,
+                         float* qbar, float* kbar, float* vbar,
+                         int B, int H, int N, int d, int block_q, int block_k,
+                         int dtype, void* stream);
+
+/*
+ * Query-dependent thresholds from pooled inputs (Section 3.1, Eq.
+ * threshold_routing with the moment form of Eq. threshold_stats_exact):
+ *   mu_i    = s * Qbar_i . mean_j(Kbar_j)
+ *   sigma_i = s * sqrt(Qbar_i C_K Qbar_i^T),  C_K the population covariance of
+ *             the routable pooled keys (centred, accumulated in f64)
+ *   tau_i   = mu_i + beta * sigma_i  (beta = -inf -> -inf, beta = +inf -> +inf)
+ * with s = 1/sqrt(d).  Only the first nk_routable pooled keys take part.
+ *
+ * qbar: [B,H,NQ,d] f32 device; kbar: [B,H,NK,d] f32 device (NK >= nk_routable,
+ * row stride d, NK rows per (b,h)).  tau (required), mu, sigma (optional):
+ * [B,H,NQ] f32 device.  beta must not be NaN.  Unlike the forward calls this
+ * entry point allocates temporary device memory for the moments and
+ * synchronises `stream` before returning.
+ */
+int sol_attn_thresholds(const float* qbar, const float* kbar,
+                        float* tau, float* mu, float* sigma,
+                        int B, int H, int NQ, int NK, int nk_routable, int d,
+                        float beta, void* stream);
+
+/*
+ * Routed attention forward, short form: bf16 q/k/v/out, default stream,
+ * library-managed workspace, per-head counts kept for sol_attn_stats().
+ * `tau` is the standardised cutoff beta of Eq. threshold_routing; mode is one
+ * of SOL_DENSE, SOL_SPARSE, SOL_SPARSE_NO_CORRECTION.
+ */
+int sol_attn_forward(const void* q, const void* k, const void* v, void* out,
+                     int B, int H, int N, int d, int block_q, int block_k,
+                     float tau, int mode);
+
+/*
+ * Routed attention forward, full form.
+ *
+ * q, k, v (in), out (out): [B,H,N,d] device, element type `dtype`; out must not
+ *   alias q, k or v.
+ * tau: standardised cutoff beta (tau_i = mu_i + beta*sigma_i per query block,
+ *   Eq. threshold_routing).  -INFINITY keeps every routable block (sparse modes
+ *   then equal dense), +INFINITY keeps none.  Ignored by SOL_DENSE.  NaN is an
+ *   error.
+ * keep_tail_tokens: the last keep_tail_tokens tokens (a multiple of block_k,
+ *   e.g. the text tokens of an MMDiT; Appendix, "Generation Configurations")
+ *   form forced key blocks that are always computed exactly and take no part
+ *   in the routing statistics or the counts.  0 for none.
+ * workspace/workspace_bytes: caller device scratch of at least
+ *   sol_attn_workspace_bytes(...) bytes, or NULL/0 to let the library allocate
+ *   (and keep, growing on demand) its own.
+ * counts: [B,H] u32 device, or NULL for a library buffer.  After the call,
+ *   counts[b*H+h] = number of (query block, routable key block) pairs selected
+ *   for exact computation (all routable pairs in SOL_DENSE).
+ * mask_out: [B,H,NQ,ceil(NKr/32)] u32 device bit mask of the selection (bit
+ *   j%32 of word j/32 for key block j), or NULL.  Debug/parity aid; not
+ *   written in SOL_DENSE.
+ * stream: hipStream_t or NULL.
+ *
+ * Selection is computed on chip from f32 pooled proxies s*Qbar_i.Kbar_j and
+ * never written to memory unless mask_out is given.
+ */
+int sol_attn_forward_ex(const void* q, const void* k, const void* v, void* out,
+                        int B, int H, int N, int d, int block_q, int block_k,
+                        float tau, int mode, int dtype, int keep_tail_tokens,
+                        void* workspace, size_t workspace_bytes,
+                        uint32_t* counts, uint32_t* mask_out, void* stream);
+
+/* Device workspace bytes sol_attn_forward_ex needs for these arguments, or 0
+ * if they are invalid/unsupported. */
+size_t sol_attn_workspace_bytes(int B, int H, int N, int d, int block_q, int block_k,
+                                int mode, int dtype, int keep_tail_tokens);
+
+/*
+ * Per-head selected-block fraction of the most recent forward call in this
+ * process: frac_per_head[b*H+h] = counts[b*H+h] / (NQ * NKr) (host float array
+ * of B*H entries).  Synchronises that call's stream.  Returns SOL_ERR_NO_DATA
+ * if there was no forward or B/H differ from it.
+ */
+int sol_attn_stats(float* frac_per_head, int B, int H);
+
+/*
+ * Kernel timing (profiling aid).  While enabled, every forward records a pair
+ * of HIP events around its fused attention kernel on the call's stream (at most
+ * 4096 launches are kept).  sol_attn_kernel_timing() waits for the recorded
+ * launches, returns their total milliseconds and count, and clears them.
+ */
+int sol_attn_timing_enable(int enable);
+int sol_attn_kernel_timing(float* total_ms, int* launches);
+
+/* Message for the last non-zero return on the calling thread ("" if none). */
+const char* sol_attn_last_error(void);
+
+/* Free library-owned workspace and counter buffers (all devices).  The next
+ * forward reallocates. */
+int sol_attn_release(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SOL_ATTN_H */

@@ -1,0 +1,191 @@
+"""ctypes binding of libsolattn.so (C ABI in include/sol_attn.h).
+
+Argument marshalling only: torch tensors supply device memory and the current
+stream; every step of the computation runs in the library's HIP kernels.  The
+library must be built (``python -m paper_2607_24027_amd.build``); loading fails
+loudly otherwise.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsolattn.so")
+
+SOL_DENSE, SOL_SPARSE, SOL_SPARSE_NO_CORRECTION = 0, 1, 2
+SOL_BF16, SOL_F32 = 0, 1
+SOL_OK, SOL_ERR_INVALID_ARG, SOL_ERR_UNSUPPORTED, SOL_ERR_HIP, SOL_ERR_WORKSPACE, SOL_ERR_NO_DATA = 0, -1, -2, -3, -4, -5
+MODES = {"dense": SOL_DENSE, "sparse": SOL_SPARSE, "sparse_no_correction": SOL_SPARSE_NO_CORRECTION}
+
+# (name, restype, argtypes) for every symbol of include/sol_attn.h
+_P, _I, _F, _S = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+SIGNATURES = {
+    "sol_attn_pool_blocks": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P]),
+    "sol_attn_thresholds": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _P]),
+    "sol_attn_forward": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I]),
+    "sol_attn_forward_ex": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _I, _I, _P, _S, _P, _P, _P]),
+    "sol_attn_workspace_bytes": (_S, [_I, _I, _I, _I, _I, _I, _I, _I, _I]),
+    "sol_attn_stats": (_I, [_P, _I, _I]),
+    "sol_attn_timing_enable": (_I, [_I]),
+    "sol_attn_kernel_timing": (_I, [_P, _P]),
+    "sol_attn_last_error": (ctypes.c_char_p, []),
+    "sol_attn_release": (_I, []),
+}
+
+_lib = None
+
+
+class SolAttnError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"sol_attn error {code}: {msg}")
+        self.code = code
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsolattn.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_24027_amd.build`")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def last_error() -> str:
+    return lib().sol_attn_last_error().decode()
+
+
+def _check(rc: int):
+    if rc != SOL_OK:
+        raise SolAttnError(rc, last_error())
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device) -> int:
+    import torch
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return SOL_BF16
+    if t.dtype == torch.float32:
+        return SOL_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _check_qkv(*ts):
+    for t in ts:
+        if t is None:
+            continue
+        if not t.is_cuda or not t.is_contiguous() or t.dim() != 4:
+            raise ValueError("tensors must be contiguous 4-D [B,H,N,d] device tensors")
+
+
+def pool_blocks(q, k, v, block_q: int, block_k: int):
+    """Block means (Qbar [B,H,NQ,d], Kbar, Vbar [B,H,NK,d], f32) of q, k, v."""
+    import torch
+    _check_qkv(q, k, v)
+    B, H, N, d = q.shape
+    nq, nk = -(-N // block_q), -(-N // block_k)
+    qbar = torch.empty((B, H, nq, d), device=q.device, dtype=torch.float32)
+    kbar = torch.empty((B, H, nk, d), device=q.device, dtype=torch.float32)
+    vbar = torch.empty((B, H, nk, d), device=q.device, dtype=torch.float32)
+    _check(lib().sol_attn_pool_blocks(_ptr(q), _ptr(k), _ptr(v), _ptr(qbar), _ptr(kbar), _ptr(vbar),
+                                      B, H, N, d, block_q, block_k, _dtype_code(q), _stream(q.device)))
+    return qbar, kbar, vbar
+
+
+def thresholds(qbar, kbar, beta: float, nk_routable: Optional[int] = None):
+    """(tau, mu, sigma) [B,H,NQ] f32 from pooled queries/keys (moment form)."""
+    import torch
+    B, H, NQ, d = qbar.shape
+    NK = kbar.shape[2]
+    nkr = NK if nk_routable is None else nk_routable
+    tau = torch.empty((B, H, NQ), device=qbar.device, dtype=torch.float32)
+    mu = torch.empty_like(tau)
+    sigma = torch.empty_like(tau)
+    _check(lib().sol_attn_thresholds(_ptr(qbar.contiguous()), _ptr(kbar.contiguous()), _ptr(tau), _ptr(mu),
+                                     _ptr(sigma), B, H, NQ, NK, nkr, d, float(beta), _stream(qbar.device)))
+    return tau, mu, sigma
+
+
+def workspace_bytes(B, H, N, d, block_q, block_k, mode, dtype=SOL_BF16, keep_tail_tokens=0) -> int:
+    return int(lib().sol_attn_workspace_bytes(B, H, N, d, block_q, block_k, MODES.get(mode, mode), dtype,
+                                              keep_tail_tokens))
+
+
+def forward(q, k, v, block_q: int, block_k: int, tau: float, mode="sparse", keep_tail_tokens: int = 0,
+            out=None, workspace=None, counts=None, mask_out=None):
+    """Routed attention forward through sol_attn_forward_ex.  Returns out."""
+    import torch
+    _check_qkv(q, k, v)
+    B, H, N, d = q.shape
+    if out is None:
+        out = torch.empty_like(q)
+    m = MODES[mode] if isinstance(mode, str) else int(mode)
+    ws_ptr, ws_bytes = (None, 0) if workspace is None else (workspace.data_ptr(), workspace.numel() * workspace.element_size())
+    _check(lib().sol_attn_forward_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, block_q, block_k,
+                                     float(tau), m, _dtype_code(q), keep_tail_tokens, ws_ptr, ws_bytes,
+                                     _ptr(counts), _ptr(mask_out), _stream(q.device)))
+    return out
+
+
+def forward_short(q, k, v, out, block_q: int, block_k: int, tau: float, mode="sparse"):
+    """The 12-argument sol_attn_forward (bf16, default stream, library workspace)."""
+    B, H, N, d = q.shape
+    m = MODES[mode] if isinstance(mode, str) else int(mode)
+    _check(lib().sol_attn_forward(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, block_q, block_k,
+                                  float(tau), m))
+    return out
+
+
+def stats(B: int, H: int):
+    """Per-head selected fraction of the last forward (host list, synchronising)."""
+    arr = (ctypes.c_float * (B * H))()
+    _check(lib().sol_attn_stats(ctypes.cast(arr, ctypes.c_void_p), B, H))
+    return [float(x) for x in arr]
+
+
+def mask_words(NKr: int) -> int:
+    return -(-NKr // 32)
+
+
+def unpack_mask(words, NKr: int):
+    """[..., MW] int32/uint32 words -> [..., NKr] bool (bit j%32 of word j//32)."""
+    import numpy as np
+    w = np.asarray(words).astype(np.uint32)
+    bits = ((w[..., :, None] >> np.arange(32, dtype=np.uint32)) & 1).astype(bool)
+    return bits.reshape(w.shape[:-1] + (w.shape[-1] * 32,))[..., :NKr]
+
+
+def timing_enable(enable: bool = True):
+    _check(lib().sol_attn_timing_enable(1 if enable else 0))
+
+
+def kernel_timing():
+    """(total_ms, launches) of the fused attention kernel since the last call."""
+    ms = ctypes.c_float()
+    n = ctypes.c_int()
+    _check(lib().sol_attn_kernel_timing(ctypes.cast(ctypes.pointer(ms), ctypes.c_void_p),
+                                        ctypes.cast(ctypes.pointer(n), ctypes.c_void_p)))
+    return float(ms.value), int(n.value)
+
+
+def release():
+    _check(lib().sol_attn_release())
+
+
+NEG_INF = -math.inf

@@ -1,0 +1,315 @@
+// C ABI of the routed-attention library: argument validation, workspace management and
+// launch sequencing.  Validation runs entirely on the host and returns before any HIP call.
+#include "../../include/sol_attn.h"
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "sol_attn_internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int ok() {
+    g_err.clear();
+    return SOL_OK;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(SOL_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Library-owned device buffers, one set per device, grown on demand.
+struct DeviceBuffers {
+    void* ws = nullptr;
+    size_t ws_bytes = 0;
+    uint32_t* counts = nullptr;
+    size_t counts_n = 0;
+};
+
+std::mutex g_mu;
+std::map<int, DeviceBuffers> g_bufs;
+
+// Record of the most recent forward, for sol_attn_stats.
+struct LastCall {
+    bool valid = false;
+    int device = 0;
+    int B = 0, H = 0, NQ = 0, NKr = 0;
+    const uint32_t* counts = nullptr;
+    hipStream_t stream = nullptr;
+};
+LastCall g_last;
+
+// Kernel timing: event pairs recorded around the fused attention kernel.
+constexpr int kMaxTimed = 4096;
+struct Timing {
+    bool enabled = false;
+    int device = -1;
+    std::vector<hipEvent_t> start, stop;
+    int used = 0;
+};
+Timing g_timing;
+
+bool finite_or_inf(float x) { return !std::isnan(x); }
+
+int check_common(int B, int H, int N, int d, int block_q, int block_k, int dtype) {
+    if (B <= 0 || H <= 0 || N <= 0) return fail(SOL_ERR_INVALID_ARG, "B, H and N must be positive (got %d, %d, %d)", B, H, N);
+    if (d <= 0 || block_q <= 0 || block_k <= 0)
+        return fail(SOL_ERR_INVALID_ARG, "d, block_q and block_k must be positive (got %d, %d, %d)", d, block_q, block_k);
+    if (dtype != SOL_BF16 && dtype != SOL_F32) return fail(SOL_ERR_INVALID_ARG, "dtype must be SOL_BF16 or SOL_F32 (got %d)", dtype);
+    if (d != 64 && d != 128) return fail(SOL_ERR_UNSUPPORTED, "d must be 64 or 128 (got %d)", d);
+    if ((long long)B * H > (1LL << 24)) return fail(SOL_ERR_UNSUPPORTED, "B*H too large");
+    if ((long long)N * d * B * H > (1LL << 40)) return fail(SOL_ERR_UNSUPPORTED, "tensor too large");
+    return SOL_OK;
+}
+
+int validate_forward(const void* q, const void* k, const void* v, const void* out, int B, int H, int N, int d,
+                     int block_q, int block_k, float tau, int mode, int dtype, int keep_tail) {
+    if (!q || !k || !v || !out) return fail(SOL_ERR_INVALID_ARG, "q, k, v and out must be non-null");
+    int rc = check_common(B, H, N, d, block_q, block_k, dtype);
+    if (rc) return rc;
+    if (mode != SOL_DENSE && mode != SOL_SPARSE && mode != SOL_SPARSE_NO_CORRECTION)
+        return fail(SOL_ERR_INVALID_ARG, "mode must be SOL_DENSE, SOL_SPARSE or SOL_SPARSE_NO_CORRECTION (got %d)", mode);
+    if (!finite_or_inf(tau)) return fail(SOL_ERR_INVALID_ARG, "tau (standardised cutoff beta) is NaN");
+    if (block_k != 64) return fail(SOL_ERR_UNSUPPORTED, "block_k must be 64 (got %d)", block_k);
+    if (block_q != 64 && block_q != 128) return fail(SOL_ERR_UNSUPPORTED, "block_q must be 64 or 128 (got %d)", block_q);
+    if (keep_tail < 0 || keep_tail % block_k) return fail(SOL_ERR_INVALID_ARG, "keep_tail_tokens must be a non-negative multiple of block_k (got %d)", keep_tail);
+    if (keep_tail >= N && mode != SOL_DENSE) return fail(SOL_ERR_INVALID_ARG, "keep_tail_tokens must leave at least one routable key block");
+    if (keep_tail > N) return fail(SOL_ERR_INVALID_ARG, "keep_tail_tokens exceeds N");
+    if (out == q || out == k || out == v) return fail(SOL_ERR_INVALID_ARG, "out must not alias q, k or v");
+    const sol::Shape s = sol::make_shape(B, H, N, d, block_q, block_k, mode, dtype, keep_tail);
+    if (sol::attn_lds_bytes(s) > (size_t)sol::kMaxLds)
+        return fail(SOL_ERR_UNSUPPORTED, "sequence too long: %d key blocks exceed the on-chip routing list", s.NK);
+    return SOL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sol_attn_last_error(void) { return g_err.c_str(); }
+
+int sol_attn_pool_blocks(const void* q, const void* k, const void* v, float* qbar, float* kbar, float* vbar, int B, int H,
+                         int N, int d, int block_q, int block_k, int dtype, void* stream) {
+    int rc = check_common(B, H, N, d, block_q, block_k, dtype);
+    if (rc) return rc;
+    if (!qbar && !kbar && !vbar) return fail(SOL_ERR_INVALID_ARG, "at least one of qbar, kbar, vbar must be non-null");
+    if ((qbar && !q) || (kbar && !k) || (vbar && !v))
+        return fail(SOL_ERR_INVALID_ARG, "an input matching a non-null output is null");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int BH = B * H;
+    hipError_t e;
+    if (qbar && (e = sol::launch_pool_mean(q, qbar, dtype, BH, N, d, block_q, st)) != hipSuccess) return hip_fail(e, "pool q");
+    if (kbar && (e = sol::launch_pool_mean(k, kbar, dtype, BH, N, d, block_k, st)) != hipSuccess) return hip_fail(e, "pool k");
+    if (vbar && (e = sol::launch_pool_mean(v, vbar, dtype, BH, N, d, block_k, st)) != hipSuccess) return hip_fail(e, "pool v");
+    return ok();
+}
+
+int sol_attn_thresholds(const float* qbar, const float* kbar, float* tau, float* mu, float* sigma, int B, int H, int NQ,
+                        int NK, int nk_routable, int d, float beta, void* stream) {
+    if (!qbar || !kbar || !tau) return fail(SOL_ERR_INVALID_ARG, "qbar, kbar and tau must be non-null");
+    if (B <= 0 || H <= 0 || NQ <= 0 || NK <= 0) return fail(SOL_ERR_INVALID_ARG, "B, H, NQ and NK must be positive");
+    if (nk_routable <= 0 || nk_routable > NK) return fail(SOL_ERR_INVALID_ARG, "nk_routable must be in [1, NK]");
+    if (d != 64 && d != 128) return fail(SOL_ERR_UNSUPPORTED, "d must be 64 or 128 (got %d)", d);
+    if (std::isnan(beta)) return fail(SOL_ERR_INVALID_ARG, "beta is NaN");
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int BH = B * H;
+    // Moment buffers are temporary: allocate, run, wait, free (this entry point synchronises).
+    void* mom = nullptr;
+    hipError_t e = hipMalloc(&mom, ((size_t)BH * d * d + (size_t)BH * d) * sizeof(float));
+    if (e != hipSuccess) return hip_fail(e, "hipMalloc(moments)");
+    float* cov = static_cast<float*>(mom);
+    float* muk = cov + (size_t)BH * d * d;
+    e = sol::launch_moments(kbar, muk, cov, BH, NK, nk_routable, d, st);
+    if (e == hipSuccess) e = sol::launch_tau(qbar, muk, cov, tau, mu, sigma, BH, NQ, d, beta, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    (void)hipFree(mom);
+    if (e != hipSuccess) return hip_fail(e, "threshold kernels");
+    return ok();
+}
+
+size_t sol_attn_workspace_bytes(int B, int H, int N, int d, int block_q, int block_k, int mode, int dtype,
+                                int keep_tail_tokens) {
+    static const char dummy = 0;
+    if (validate_forward(&dummy, &dummy + 1, &dummy + 2, &dummy + 3, B, H, N, d, block_q, block_k, 0.f, mode, dtype,
+                         keep_tail_tokens) != SOL_OK)
+        return 0;
+    const sol::Shape s = sol::make_shape(B, H, N, d, block_q, block_k, mode, dtype, keep_tail_tokens);
+    return sol::workspace_layout(s, nullptr, nullptr);
+}
+
+int sol_attn_forward_ex(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d, int block_q,
+                        int block_k, float tau, int mode, int dtype, int keep_tail_tokens, void* workspace,
+                        size_t workspace_bytes, uint32_t* counts, uint32_t* mask_out, void* stream) {
+    int rc = validate_forward(q, k, v, out, B, H, N, d, block_q, block_k, tau, mode, dtype, keep_tail_tokens);
+    if (rc) return rc;
+    const sol::Shape s = sol::make_shape(B, H, N, d, block_q, block_k, mode, dtype, keep_tail_tokens);
+    const size_t need = sol::workspace_layout(s, nullptr, nullptr);
+    if (workspace && workspace_bytes < need)
+        return fail(SOL_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu bytes required", workspace_bytes, need);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+
+    std::lock_guard<std::mutex> lock(g_mu);
+    DeviceBuffers& db = g_bufs[dev];
+    if (!workspace) {
+        if (db.ws_bytes < need) {
+            if (db.ws) {
+                e = hipDeviceSynchronize();
+                if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+                (void)hipFree(db.ws);
+                db.ws = nullptr;
+                db.ws_bytes = 0;
+            }
+            e = hipMalloc(&db.ws, need);
+            if (e != hipSuccess) return hip_fail(e, "hipMalloc(workspace)");
+            db.ws_bytes = need;
+        }
+        workspace = db.ws;
+    }
+    if (!counts) {
+        const size_t n = (size_t)s.BH;
+        if (db.counts_n < n) {
+            if (db.counts) {
+                e = hipDeviceSynchronize();
+                if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+                (void)hipFree(db.counts);
+                db.counts = nullptr;
+                db.counts_n = 0;
+            }
+            e = hipMalloc(reinterpret_cast<void**>(&db.counts), n * sizeof(uint32_t));
+            if (e != hipSuccess) return hip_fail(e, "hipMalloc(counts)");
+            db.counts_n = n;
+        }
+        counts = db.counts;
+    }
+    sol::Workspace ws;
+    sol::workspace_layout(s, static_cast<char*>(workspace), &ws);
+    hipEvent_t ev0 = nullptr, ev1 = nullptr;
+    if (g_timing.enabled && g_timing.device == dev && g_timing.used < kMaxTimed) {
+        ev0 = g_timing.start[g_timing.used];
+        ev1 = g_timing.stop[g_timing.used];
+        ++g_timing.used;
+    }
+    e = sol::launch_forward(s, q, k, v, out, tau, ws, counts, mask_out, st, ev0, ev1);
+    if (e != hipSuccess) return hip_fail(e, "forward launch");
+    g_last.valid = true;
+    g_last.device = dev;
+    g_last.B = B;
+    g_last.H = H;
+    g_last.NQ = s.NQ;
+    g_last.NKr = s.NKr;
+    g_last.counts = counts;
+    g_last.stream = st;
+    return ok();
+}
+
+int sol_attn_forward(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d, int block_q,
+                     int block_k, float tau, int mode) {
+    return sol_attn_forward_ex(q, k, v, out, B, H, N, d, block_q, block_k, tau, mode, SOL_BF16, 0, nullptr, 0, nullptr,
+                               nullptr, nullptr);
+}
+
+int sol_attn_stats(float* frac_per_head, int B, int H) {
+    if (!frac_per_head) return fail(SOL_ERR_INVALID_ARG, "frac_per_head must be non-null");
+    LastCall last;
+    {
+        std::lock_guard<std::mutex> lock(g_mu);
+        last = g_last;
+    }
+    if (!last.valid) return fail(SOL_ERR_NO_DATA, "no forward call has been made");
+    if (last.B != B || last.H != H)
+        return fail(SOL_ERR_NO_DATA, "B/H (%d, %d) differ from the last forward (%d, %d)", B, H, last.B, last.H);
+    int cur = 0;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (cur != last.device && (e = hipSetDevice(last.device)) != hipSuccess) return hip_fail(e, "hipSetDevice");
+    const size_t n = (size_t)B * H;
+    uint32_t* host = new uint32_t[n];
+    e = hipStreamSynchronize(last.stream);
+    if (e == hipSuccess) e = hipMemcpy(host, last.counts, n * sizeof(uint32_t), hipMemcpyDeviceToHost);
+    if (cur != last.device) (void)hipSetDevice(cur);
+    if (e != hipSuccess) {
+        delete[] host;
+        return hip_fail(e, "reading counts");
+    }
+    const double denom = (double)last.NQ * (double)last.NKr;
+    for (size_t i = 0; i < n; ++i) frac_per_head[i] = (float)((double)host[i] / denom);
+    delete[] host;
+    return ok();
+}
+
+int sol_attn_timing_enable(int enable) {
+    std::lock_guard<std::mutex> lock(g_mu);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (enable && g_timing.start.empty()) {
+        g_timing.start.resize(kMaxTimed);
+        g_timing.stop.resize(kMaxTimed);
+        for (int i = 0; i < kMaxTimed; ++i) {
+            if ((e = hipEventCreate(&g_timing.start[i])) != hipSuccess) return hip_fail(e, "hipEventCreate");
+            if ((e = hipEventCreate(&g_timing.stop[i])) != hipSuccess) return hip_fail(e, "hipEventCreate");
+        }
+        g_timing.device = dev;
+    }
+    if (enable && g_timing.device != dev) return fail(SOL_ERR_UNSUPPORTED, "timing events belong to device %d", g_timing.device);
+    g_timing.enabled = enable != 0;
+    g_timing.used = 0;
+    return ok();
+}
+
+int sol_attn_kernel_timing(float* total_ms, int* launches) {
+    if (!total_ms || !launches) return fail(SOL_ERR_INVALID_ARG, "total_ms and launches must be non-null");
+    std::lock_guard<std::mutex> lock(g_mu);
+    double total = 0.0;
+    for (int i = 0; i < g_timing.used; ++i) {
+        hipError_t e = hipEventSynchronize(g_timing.stop[i]);
+        if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+        float ms = 0.f;
+        e = hipEventElapsedTime(&ms, g_timing.start[i], g_timing.stop[i]);
+        if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+        total += ms;
+    }
+    *total_ms = (float)total;
+    *launches = g_timing.used;
+    g_timing.used = 0;
+    return ok();
+}
+
+int sol_attn_release(void) {
+    std::lock_guard<std::mutex> lock(g_mu);
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    for (auto& kv : g_bufs) {
+        (void)hipSetDevice(kv.first);
+        (void)hipDeviceSynchronize();
+        if (kv.second.ws) (void)hipFree(kv.second.ws);
+        if (kv.second.counts) (void)hipFree(kv.second.counts);
+        kv.second = DeviceBuffers{};
+    }
+    (void)hipSetDevice(cur);
+    g_bufs.clear();
+    g_last = LastCall{};
+    return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,59 @@
+// Internal interface between the C ABI (sol_attn_api.cpp) and the gfx950
+// kernels (sol_attn_kernels.hip).  Not installed; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace sol {
+
+constexpr int kBlockK = 64;        // key block size (rows of one exact K/V tile)
+constexpr int kChunk = 64;         // pooled keys per correction tile
+constexpr int kMaxLds = 160 * 1024;
+
+enum Mode { kDense = 0, kSparse = 1, kSparseNoCorr = 2 };
+enum DType { kBF16 = 0, kF32 = 1 };
+
+// Derived sizes of one forward call.
+struct Shape {
+    int B, H, N, d, bq, bk;
+    int mode, dtype, forced;       // forced = number of always-exact tail key blocks
+    int BH, NQ, NK, NKr, NC, Npad, MW;
+};
+
+Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype, int keep_tail_tokens);
+
+// Workspace carve-up (all device pointers, 256-byte aligned inside one buffer).
+struct Workspace {
+    float* qbar = nullptr;       // [BH][NQ][d]
+    float* kbar = nullptr;       // [BH][NK][d]
+    float* vbar = nullptr;       // [BH][NK][d]            (f32 path)
+    uint16_t* kbar16 = nullptr;  // [BH][NC*64][d] bf16     (bf16 sparse)
+    _Float16* vbart = nullptr;   // [BH][NC][d][64] f16     (bf16 sparse)
+    _Float16* vt = nullptr;      // [BH][d][Npad] f16       (bf16)
+    float* muk = nullptr;        // [BH][d]
+    float* cov = nullptr;        // [BH][d][d]
+    float* tau = nullptr;        // [BH][NQ]
+    uint32_t* blkcount = nullptr;// [BH][NQ]
+};
+
+// Returns the byte size; fills *ws when base != nullptr.
+size_t workspace_layout(const Shape& s, char* base, Workspace* ws);
+
+// Dynamic LDS bytes of the fused attention kernel for this shape.
+size_t attn_lds_bytes(const Shape& s);
+
+hipError_t launch_pool_mean(const void* x, float* mean, int dtype, int BH, int N, int d, int blk,
+                            hipStream_t st);
+hipError_t launch_moments(const float* kbar, float* muk, float* cov, int BH, int NK, int NKr, int d,
+                          hipStream_t st);
+hipError_t launch_tau(const float* qbar, const float* muk, const float* cov, float* tau, float* mu,
+                      float* sigma, int BH, int NQ, int d, float beta, hipStream_t st);
+// ev_start/ev_stop (nullable) are recorded on `st` around the fused attention kernel.
+hipError_t launch_forward(const Shape& s, const void* q, const void* k, const void* v, void* out,
+                          float beta, const Workspace& ws, uint32_t* counts, uint32_t* mask_out,
+                          hipStream_t st, hipEvent_t ev_start = nullptr, hipEvent_t ev_stop = nullptr);
+
+}  // namespace sol

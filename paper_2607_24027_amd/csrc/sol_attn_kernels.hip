@@ -1,0 +1,1048 @@
+// gfx950 kernels of the Sol-Attn forward pass.
+//
+// Pipeline of one forward (bf16 inputs):
+//   1. pool_mean      Qbar_i = token mean of query block i           (Eq. block_proxy)
+//   2. prep_kv        Kbar_j (f32 + bf16 copy), Vbar_j (f16, correction layout) and the
+//                     f16 transposed V used by the exact tiles
+//   3. moments        mean and centred covariance of the routable pooled keys, f64 sums
+//   4. tau            tau_i = mu_i + beta*sigma_i from the moments   (Eqs. threshold_routing,
+//                                                                       threshold_stats_exact)
+//   5. routed_attn    one workgroup per (b, h, query block): routes every key block on chip
+//                     from f32 proxies, then runs one online-softmax pass over correction
+//                     tiles (pooled keys, Section 3.2 "Proxy-Score Reuse") and exact tiles
+//                     (selected key blocks), with bf16 MFMA for QK^T and f16 MFMA for PV
+//   6. count_reduce   per-head number of selected routable pairs
+//
+// Tile math (wave64, v_mfma_f32_32x32x16_{bf16,f16}): each wave owns 32 query rows and
+// computes the transposed score tile S^T = K Q^T (keys on MFMA rows, queries on lanes), so a
+// query's softmax state lives in one lane pair (l, l+32).  The probabilities are fed straight
+// from the accumulator registers as the B operand of O^T += V^T P^T; for that the transposed
+// V tiles store each 16-key segment with its two middle 4-key groups swapped, which makes the
+// 8 keys a lane contributes contiguous in LDS.
+#include "sol_attn_internal.h"
+
+#include <cmath>
+
+namespace sol {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kNegInf = -__builtin_huge_valf();
+constexpr float kLog2e = 1.4426950408889634f;
+// Lazy rescaling: the running max subtracted from the logits (log2 units) is only raised
+// when a tile's max exceeds it by more than this, so probabilities stay <= 2^8 (f16-safe).
+constexpr float kRescaleSlack = 8.0f;
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t bits16) {
+    return __uint_as_float(bits16 << 16);
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) {
+    return __builtin_bit_cast(uint16_t, (__bf16)x);
+}
+
+// Position p of a transposed V row holds key swap23(p): bits 2 and 3 exchanged.
+__device__ __forceinline__ int swap23(int p) {
+    return (p & ~12) | ((p & 8) >> 1) | ((p & 4) << 1);
+}
+
+template <typename T>
+struct Elem;
+template <>
+struct Elem<uint16_t> {
+    static constexpr int kPerChunk = 8;
+    __device__ static void unpack(const u32x4& c, float* out) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            out[2 * e] = bf16_bits_to_f32(c[e] & 0xffffu);
+            out[2 * e + 1] = bf16_bits_to_f32(c[e] >> 16);
+        }
+    }
+};
+template <>
+struct Elem<float> {
+    static constexpr int kPerChunk = 4;
+    __device__ static void unpack(const u32x4& c, float* out) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) out[e] = __uint_as_float(c[e]);
+    }
+};
+
+// ---------------------------------------------------------------------------
+// Block mean pooling.  grid (nblocks, BH), 256 threads.  Each thread sums 16-byte
+// chunks of a fixed column group over a strided set of rows; row groups are then
+// combined through LDS.  Only the block's valid rows are read.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void pool_mean_kernel(const T* __restrict__ x, float* __restrict__ mean,
+                                                        int N, int D, int blk, int nb) {
+    constexpr int EPC = Elem<T>::kPerChunk;
+    __shared__ float red[256 * EPC];
+    const int j = blockIdx.x, bh = blockIdx.y, t = threadIdx.x;
+    const int cpr = D / EPC;
+    const int groups = 256 / cpr;
+    const int cc = t % cpr, g = t / cpr;
+    const int row0 = j * blk;
+    const int n = min(blk, N - row0);
+    const T* base = x + ((size_t)bh * N + row0) * D + cc * EPC;
+    float acc[EPC];
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
+    for (int r = g; r < n; r += groups) {
+        u32x4 c = *reinterpret_cast<const u32x4*>(base + (size_t)r * D);
+        float f[EPC];
+        Elem<T>::unpack(c, f);
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) acc[e] += f[e];
+    }
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) red[g * D + cc * EPC + e] = acc[e];
+    __syncthreads();
+    const float inv = 1.0f / (float)n;
+    for (int c = t; c < D; c += 256) {
+        float s = 0.f;
+        for (int gg = 0; gg < groups; ++gg) s += red[gg * D + c];
+        mean[((size_t)bh * nb + j) * D + c] = s * inv;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// K/V preparation for the bf16 forward.  grid (NJ, BH), 256 threads, one key block each.
+//   vt     [BH][D][Npad] f16: V^T with swap23 key order inside each 16-key segment; rows
+//          past N are zero.
+//   routing modes additionally:
+//   kbar   [BH][NK][D] f32 means (routing proxies and moments)
+//   kbar16 [BH][NC*64][D] bf16 means of routable blocks (A operand of correction tiles);
+//          zero for forced and padding rows
+//   vbart  [BH][NC][D][64] f16 value means in correction layout (slot swap23(j%64));
+//          zero for forced and padding slots
+// Blocks j >= NK exist only to zero the padding rows of the last correction tile.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+                                                      float* __restrict__ kbar, uint16_t* __restrict__ kbar16,
+                                                      _Float16* __restrict__ vbart, _Float16* __restrict__ vt,
+                                                      int N, int NK, int NKr, int NC, int Npad, int routing) {
+    constexpr int CPR = D / 8;          // 16-byte chunks per row
+    constexpr int GROUPS = 256 / CPR;   // row groups
+    constexpr int VS = D + 2;           // f16 row stride of the staged V tile (odd word count)
+    __shared__ _Float16 vtile[kBlockK * VS];
+    __shared__ float red[GROUPS * D];
+    const int j = blockIdx.x, bh = blockIdx.y, t = threadIdx.x;
+    const int cc = t % CPR, g = t / CPR;
+
+    if (j >= NK) {  // padding rows of the last correction tile
+        for (int c = t; c < D; c += 256) {
+            kbar16[((size_t)bh * NC * kChunk + j) * D + c] = 0;
+            vbart[(((size_t)bh * NC + j / kChunk) * D + c) * kChunk + swap23(j % kChunk)] = (_Float16)0.f;
+        }
+        return;
+    }
+    const int row0 = j * kBlockK;
+    const int n = min(kBlockK, N - row0);
+    const float inv = 1.0f / (float)n;
+
+    // ---- V: stage as f16 (exact for bf16 values inside the f16 range) and sum columns
+    {
+        const uint16_t* base = v + ((size_t)bh * N + row0) * D + cc * 8;
+        float acc[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+        for (int r = g; r < kBlockK; r += GROUPS) {
+            float f[8];
+            if (r < n) {
+                u32x4 c = *reinterpret_cast<const u32x4*>(base + (size_t)r * D);
+                Elem<uint16_t>::unpack(c, f);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) f[e] = 0.f;
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                acc[e] += f[e];
+                vtile[r * VS + cc * 8 + e] = (_Float16)f[e];
+            }
+        }
+        if (routing) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) red[g * D + cc * 8 + e] = acc[e];
+        }
+    }
+    __syncthreads();
+    // transposed write: thread -> (d row, run of consecutive positions)
+    {
+        constexpr int TPR = 256 / D;             // threads per d row (2 or 4)
+        constexpr int RUN = kBlockK / TPR;       // positions per thread (32 or 16)
+        const int drow = t / TPR, p0 = (t % TPR) * RUN;
+        _Float16* dst = vt + ((size_t)bh * D + drow) * Npad + row0 + p0;
+#pragma unroll
+        for (int u = 0; u < RUN; u += 8) {
+            f16x8 pk;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pk[e] = vtile[swap23(p0 + u + e) * VS + drow];
+            *reinterpret_cast<f16x8*>(dst + u) = pk;
+        }
+    }
+    if (!routing) return;
+    if (t < D && j < NC * kChunk) {
+        float s = 0.f;
+        for (int gg = 0; gg < GROUPS; ++gg) s += red[gg * D + t];
+        const bool routable = j < NKr;
+        vbart[(((size_t)bh * NC + j / kChunk) * D + t) * kChunk + swap23(j % kChunk)] =
+            routable ? (_Float16)(s * inv) : (_Float16)0.f;
+    }
+    __syncthreads();
+    // ---- K: column means
+    {
+        const uint16_t* base = k + ((size_t)bh * N + row0) * D + cc * 8;
+        float acc[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+        for (int r = g; r < n; r += GROUPS) {
+            u32x4 c = *reinterpret_cast<const u32x4*>(base + (size_t)r * D);
+            float f[8];
+            Elem<uint16_t>::unpack(c, f);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[e] += f[e];
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) red[g * D + cc * 8 + e] = acc[e];
+    }
+    __syncthreads();
+    if (t < D) {
+        float s = 0.f;
+        for (int gg = 0; gg < GROUPS; ++gg) s += red[gg * D + t];
+        const float m = s * inv;
+        kbar[((size_t)bh * NK + j) * D + t] = m;
+        if (j < NC * kChunk)
+            kbar16[((size_t)bh * NC * kChunk + j) * D + t] = j < NKr ? f32_to_bf16_bits(m) : (uint16_t)0;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Moments of the routable pooled keys (Eq. threshold_stats_exact, centred form).
+// grid (D/16, BH), 256 threads.  Every workgroup recomputes mu_K (f64 column sums) and then
+// owns 16 rows of C_K = mean_j (Kbar_j - mu_K)^T (Kbar_j - mu_K), accumulated in f64 from
+// 64-row slabs staged in LDS.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void moments_kernel(const float* __restrict__ kbar, float* __restrict__ muk,
+                                                      float* __restrict__ cov, int NK, int NKr) {
+    constexpr int SLAB = 64;
+    constexpr int TS = D + 1;
+    __shared__ float tile[SLAB * TS];
+    __shared__ double mu_s[D];
+    const int g = blockIdx.x, bh = blockIdx.y, t = threadIdx.x;
+    const float* kb = kbar + (size_t)bh * NK * D;
+
+    // pass 1: mean
+    double colsum = 0.0;
+    for (int j0 = 0; j0 < NKr; j0 += SLAB) {
+        const int rows = min(SLAB, NKr - j0);
+        for (int e = t; e < rows * D; e += 256) tile[(e / D) * TS + e % D] = kb[(size_t)(j0 + e / D) * D + e % D];
+        __syncthreads();
+        if (t < D)
+            for (int r = 0; r < rows; ++r) colsum += (double)tile[r * TS + t];
+        __syncthreads();
+    }
+    if (t < D) mu_s[t] = colsum / (double)NKr;
+    __syncthreads();
+    if (g == 0 && t < D) muk[(size_t)bh * D + t] = (float)mu_s[t];
+
+    // pass 2: centred second moment, rows [16g, 16g+16)
+    constexpr int CPT = D / 16;  // columns per thread
+    const int r = 16 * g + t / 16, c0 = (t % 16) * CPT;
+    double acc[CPT];
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) acc[e] = 0.0;
+    for (int j0 = 0; j0 < NKr; j0 += SLAB) {
+        const int rows = min(SLAB, NKr - j0);
+        for (int e = t; e < rows * D; e += 256)
+            tile[(e / D) * TS + e % D] = (float)((double)kb[(size_t)(j0 + e / D) * D + e % D] - mu_s[e % D]);
+        __syncthreads();
+        for (int jj = 0; jj < rows; ++jj) {
+            const double a = tile[jj * TS + r];
+#pragma unroll
+            for (int e = 0; e < CPT; ++e) acc[e] += a * (double)tile[jj * TS + c0 + e];
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) cov[((size_t)bh * D + r) * D + c0 + e] = (float)(acc[e] / (double)NKr);
+}
+
+// ---------------------------------------------------------------------------
+// Thresholds (Eq. threshold_routing with Eq. threshold_stats_exact).  grid (ceil(NQ/16), BH),
+// 256 threads; C_K staged in LDS.  256/D query blocks are processed at a time, D threads
+// each: thread r forms (C_K Qbar_i^T)_r, then sums over r give Qbar_i C_K Qbar_i^T.
+// ---------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void tau_kernel(const float* __restrict__ qbar, const float* __restrict__ muk,
+                                                  const float* __restrict__ cov, float* __restrict__ tau,
+                                                  float* __restrict__ mu_out, float* __restrict__ sigma_out,
+                                                  int NQ, float beta, float scale) {
+    constexpr int QPB = 16;
+    constexpr int PAR = 256 / D;
+    extern __shared__ float smem_tau[];
+    float* C = smem_tau;              // D*D
+    float* qs = C + D * D;            // QPB*D
+    float* mk = qs + QPB * D;         // D
+    float* red = mk + D;              // 2 * 4 (partials per wave)
+    const int bh = blockIdx.y, i0 = blockIdx.x * QPB, t = threadIdx.x;
+    const int nq = min(QPB, NQ - i0);
+    for (int e = t; e < D * D; e += 256) C[e] = cov[(size_t)bh * D * D + e];
+    for (int e = t; e < nq * D; e += 256) qs[e] = qbar[((size_t)bh * NQ + i0) * D + e];
+    for (int e = t; e < D; e += 256) mk[e] = muk[(size_t)bh * D + e];
+    __syncthreads();
+    const int which = t / D, r = t % D, lane = t & 63, wave = t >> 6;
+    for (int b = 0; b < QPB; b += PAR) {
+        const int qi = b + which;
+        float w = 0.f, m = 0.f;
+        if (qi < nq) {
+            float y = 0.f;
+            for (int c = 0; c < D; ++c) y += C[c * D + r] * qs[qi * D + c];  // C_K is symmetric
+            w = qs[qi * D + r] * y;
+            m = qs[qi * D + r] * mk[r];
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+            w += __shfl_xor(w, off);
+            m += __shfl_xor(m, off);
+        }
+        if (lane == 0) {
+            red[wave * 2] = w;
+            red[wave * 2 + 1] = m;
+        }
+        __syncthreads();
+        if (r == 0 && qi < nq) {
+            constexpr int WPG = D / 64;  // waves per query block
+            float ws = 0.f, ms = 0.f;
+            for (int u = 0; u < WPG; ++u) {
+                ws += red[(wave + u) * 2];
+                ms += red[(wave + u) * 2 + 1];
+            }
+            const float mu = scale * ms;
+            const float sigma = scale * sqrtf(fmaxf(ws, 0.f));
+            float th;
+            if (beta == kNegInf) th = kNegInf;
+            else if (beta == -kNegInf) th = -kNegInf;
+            else th = mu + beta * sigma;
+            const size_t o = (size_t)bh * NQ + i0 + qi;
+            tau[o] = th;
+            if (mu_out) mu_out[o] = mu;
+            if (sigma_out) sigma_out[o] = sigma;
+        }
+        __syncthreads();
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Routing prologue shared by both attention kernels: selection bits of every routable key
+// block for query block qi into selw (LDS), then the ordered tile list:
+//   for each chunk c of 64 routable blocks: [correction tile c if it has an unselected
+//   valid block, sparse mode only] + exact tiles of its selected blocks; then forced blocks.
+// Correction tiles are encoded as kApxFlag | c.  Returns the list length; *nsel receives the
+// number of selected routable blocks.
+// ---------------------------------------------------------------------------
+constexpr int kApxFlag = 1 << 30;
+
+template <int NT>
+__device__ int block_scan_incl(int v, int* scratch, int* total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    constexpr int NW = NT / 64;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        int y = __shfl_up(v, off);
+        if (lane >= off) v += y;
+    }
+    if (lane == 63) scratch[wave] = v;
+    __syncthreads();
+    int pre = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+        const int s = scratch[w];
+        if (w < wave) pre += s;
+        tot += s;
+    }
+    __syncthreads();
+    *total = tot;
+    return v + pre;
+}
+
+template <int D, int NT, int MODE>
+__device__ int route_and_list(const float* __restrict__ qbar_i, const float* __restrict__ kbar_h, float tau_i,
+                              float scale, int NKr, int NK, int MW, int NC, float* qb_s, uint32_t* selw,
+                              int* list, int* scan_scratch, int* nsel) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    for (int c = tid; c < D; c += NT) qb_s[c] = qbar_i[c];
+    __syncthreads();
+    for (int base = 0; base < NKr; base += NT) {
+        const int j = base + tid;
+        bool sel = false;
+        if (j < NKr) {
+            const f32x4* kp = reinterpret_cast<const f32x4*>(kbar_h + (size_t)j * D);
+            float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll 8
+            for (int c4 = 0; c4 < D / 4; ++c4) {
+                const f32x4 kv = kp[c4];
+                a0 = fmaf(qb_s[4 * c4 + 0], kv[0], a0);
+                a1 = fmaf(qb_s[4 * c4 + 1], kv[1], a1);
+                a2 = fmaf(qb_s[4 * c4 + 2], kv[2], a2);
+                a3 = fmaf(qb_s[4 * c4 + 3], kv[3], a3);
+            }
+            sel = scale * ((a0 + a1) + (a2 + a3)) > tau_i;
+        }
+        const uint64_t bal = __ballot(sel);
+        if (lane == 0) {
+            const int w0 = (base + wave * 64) >> 5;
+            if (w0 < MW) selw[w0] = (uint32_t)bal;
+            if (w0 + 1 < MW) selw[w0 + 1] = (uint32_t)(bal >> 32);
+        }
+    }
+    __syncthreads();
+    int running = 0, nsel_tot = 0;
+    for (int c0 = 0; c0 < NC; c0 += NT) {
+        const int c = c0 + tid;
+        uint64_t bits = 0;
+        int ns = 0, apx = 0;
+        if (c < NC) {
+            const uint32_t lo = selw[2 * c];
+            const uint32_t hi = (2 * c + 1 < MW) ? selw[2 * c + 1] : 0u;
+            bits = (uint64_t)lo | ((uint64_t)hi << 32);
+            ns = __popcll(bits);
+            const int valid = min(kChunk, NKr - c * kChunk);
+            apx = (MODE == kSparse && ns < valid) ? 1 : 0;
+        }
+        int tot;
+        const int packed = (ns + apx) | (ns << 16);
+        const int incl = block_scan_incl<NT>(packed, scan_scratch, &tot);
+        int pos = running + (incl & 0xffff) - (ns + apx);
+        if (c < NC) {
+            if (apx) list[pos++] = kApxFlag | c;
+            while (bits) {
+                const int b = __builtin_ctzll(bits);
+                bits &= bits - 1;
+                list[pos++] = c * kChunk + b;
+            }
+        }
+        running += tot & 0xffff;
+        nsel_tot += tot >> 16;
+    }
+    for (int j = NKr + tid; j < NK; j += NT) list[running + (j - NKr)] = j;
+    __syncthreads();
+    *nsel = nsel_tot;
+    return running + (NK - NKr);
+}
+
+// ---------------------------------------------------------------------------
+// Fused routed attention, bf16 inputs.
+// ---------------------------------------------------------------------------
+struct AttnArgs {
+    const uint16_t* q;
+    const uint16_t* k;
+    const _Float16* vt;
+    const float* qbar;
+    const float* kbar;
+    const uint16_t* kbar16;
+    const _Float16* vbart;
+    const float* tau;
+    uint16_t* out;
+    uint32_t* blkcount;
+    uint32_t* mask_out;
+    int BH, N, NQ, NK, NKr, Npad, NC, MW, per_x;
+    float scale, c_log2;
+};
+
+template <int D>
+struct TileLds {
+    static constexpr int KS = D + 8;          // bf16 K row stride (elements): 16-byte pad
+    static constexpr int VS = kBlockK + 8;    // f16 V^T row stride (elements): 16-byte pad
+    static constexpr int KBYTES = kBlockK * KS * 2;
+    static constexpr int VBYTES = D * VS * 2;
+    static constexpr int STAGE = KBYTES + VBYTES;
+};
+
+template <int D, int BQ, int MODE>
+__global__ __launch_bounds__(BQ * 2) void routed_attn_kernel(AttnArgs a) {
+    constexpr int NT = BQ * 2;            // 64 threads per 32 query rows
+    constexpr int KCH = kBlockK * D * 2 / 16 / NT;   // 16-byte K chunks per thread
+    constexpr int VCH = D * kBlockK * 2 / 16 / NT;   // 16-byte V^T chunks per thread
+    constexpr int KS = TileLds<D>::KS, VS = TileLds<D>::VS;
+    constexpr int NDT = D / 32;           // output M-tiles (d rows)
+    constexpr int NKS = D / 16;           // k-steps of QK^T
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+
+    // XCD-aware mapping: consecutive workgroups go round-robin to the 8 XCDs, so XCD x gets
+    // a contiguous range of query blocks of the current head.
+    const int wg = blockIdx.x;
+    const int xcd = wg & 7, y = wg >> 3;
+    const int bh = y / a.per_x;
+    const int qi = xcd * a.per_x + (y % a.per_x);
+    if (bh >= a.BH || qi >= a.NQ) return;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int r32 = lane & 31, hh = lane >> 5;
+
+    auto kbuf = [&](int b) { return reinterpret_cast<uint16_t*>(smem + b * TileLds<D>::STAGE); };
+    auto vbuf = [&](int b) { return reinterpret_cast<_Float16*>(smem + b * TileLds<D>::STAGE + TileLds<D>::KBYTES); };
+    char* rest = smem + 2 * TileLds<D>::STAGE;
+    int* scan_scratch = reinterpret_cast<int*>(rest);
+    float* qb_s = reinterpret_cast<float*>(rest + 64);
+    uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64 + 4 * D);
+    int* list = reinterpret_cast<int*>(rest + 64 + 4 * D + 4 * ((a.MW + 3) & ~3));
+
+    int ntiles, nsel;
+    if (MODE == kDense) {
+        ntiles = a.NK;
+        nsel = a.NKr;
+    } else {
+        ntiles = route_and_list<D, NT, MODE>(a.qbar + ((size_t)bh * a.NQ + qi) * D, a.kbar + (size_t)bh * a.NK * D,
+                                             a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, qb_s,
+                                             selw, list, scan_scratch, &nsel);
+        if (a.mask_out)
+            for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
+    }
+    if (tid == 0) a.blkcount[(size_t)bh * a.NQ + qi] = (uint32_t)nsel;
+
+    // Q fragment (B operand of S^T = K Q^T): lane holds row r32 of its wave, d-range 8*hh.
+    bf16x8 qf[NKS];
+    {
+        const int row = qi * BQ + wave * 32 + r32;
+        if (row < a.N) {
+            const uint16_t* qp = a.q + ((size_t)bh * a.N + row) * D + 8 * hh;
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) qf[ks] = *reinterpret_cast<const bf16x8*>(qp + 16 * ks);
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) qf[ks] = bf16x8{};
+        }
+    }
+
+    f32x16 o[NDT];
+#pragma unroll
+    for (int mt = 0; mt < NDT; ++mt) o[mt] = f32x16{};
+    float m_run = kNegInf, l_run = 0.f;
+
+    u32x4 kr[KCH], vr[VCH];
+    auto tile_code = [&](int n) -> int { return MODE == kDense ? n : list[n]; };
+    auto fetch = [&](int code) {
+        const uint16_t* kp;
+        const _Float16* vp;
+        int nrows;
+        size_t vstride;
+        if (code & kApxFlag) {
+            const int c = code & ~kApxFlag;
+            kp = a.kbar16 + ((size_t)bh * a.NC * kChunk + (size_t)c * kChunk) * D;
+            vp = a.vbart + ((size_t)bh * a.NC + c) * D * kChunk;
+            nrows = kChunk;
+            vstride = kChunk;
+        } else {
+            kp = a.k + ((size_t)bh * a.N + (size_t)code * kBlockK) * D;
+            vp = a.vt + (size_t)bh * D * a.Npad + (size_t)code * kBlockK;
+            nrows = min(kBlockK, a.N - code * kBlockK);
+            vstride = a.Npad;
+        }
+#pragma unroll
+        for (int u = 0; u < KCH; ++u) {
+            const int ch = tid + u * NT, row = ch / (D / 8), c8 = ch % (D / 8);
+            kr[u] = row < nrows ? *reinterpret_cast<const u32x4*>(kp + (size_t)row * D + c8 * 8) : u32x4{};
+        }
+#pragma unroll
+        for (int u = 0; u < VCH; ++u) {
+            const int ch = tid + u * NT, drow = ch / 8, p8 = ch % 8;
+            vr[u] = *reinterpret_cast<const u32x4*>(vp + (size_t)drow * vstride + p8 * 8);
+        }
+    };
+    auto stash = [&](int buf) {
+#pragma unroll
+        for (int u = 0; u < KCH; ++u) {
+            const int ch = tid + u * NT, row = ch / (D / 8), c8 = ch % (D / 8);
+            *reinterpret_cast<u32x4*>(kbuf(buf) + row * KS + c8 * 8) = kr[u];
+        }
+#pragma unroll
+        for (int u = 0; u < VCH; ++u) {
+            const int ch = tid + u * NT, drow = ch / 8, p8 = ch % 8;
+            *reinterpret_cast<u32x4*>(vbuf(buf) + drow * VS + p8 * 8) = vr[u];
+        }
+    };
+
+    if (ntiles > 0) {
+        fetch(tile_code(0));
+        stash(0);
+    }
+    __syncthreads();
+
+    const float cl = a.c_log2;
+    for (int n = 0; n < ntiles; ++n) {
+        const int code = tile_code(n);
+        const int buf = n & 1;
+        const bool more = n + 1 < ntiles;
+        if (more) fetch(tile_code(n + 1));
+
+        const uint16_t* Kb = kbuf(buf);
+        const _Float16* Vb = vbuf(buf);
+
+        // ---- S^T = K Q^T  (two 32-key M-tiles)
+        f32x16 s0 = f32x16{}, s1 = f32x16{};
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+            const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(Kb + r32 * KS + 16 * ks + 8 * hh);
+            const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(Kb + (32 + r32) * KS + 16 * ks + 8 * hh);
+            s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[ks], s0, 0, 0, 0);
+            s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[ks], s1, 0, 0, 0);
+        }
+
+        // ---- masks: ragged last key block, or correction-tile multiplicity / exclusion
+        if (code & kApxFlag) {
+            const int c = code & ~kApxFlag;
+            auto apx_bias = [&](int j) -> float {  // log2(n_j) in raw-logit units, or -inf
+                bool ok = j < a.NKr;
+                if (ok) ok = !((selw[j >> 5] >> (j & 31)) & 1u);
+                const int nj = min(kBlockK, a.N - j * kBlockK);
+                return ok ? __log2f((float)nj) / cl : kNegInf;
+            };
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int slot0 = 8 * (r >> 2) + 4 * hh + (r & 3);
+                s0[r] += apx_bias(c * kChunk + slot0);
+                s1[r] += apx_bias(c * kChunk + 32 + slot0);
+            }
+        } else {
+            const int nvalid = a.N - code * kBlockK;
+            if (nvalid < kBlockK) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int key0 = 8 * (r >> 2) + 4 * hh + (r & 3);
+                    if (key0 >= nvalid) s0[r] = kNegInf;
+                    if (32 + key0 >= nvalid) s1[r] = kNegInf;
+                }
+            }
+        }
+
+        // ---- online softmax (log2 domain, lazy rescale)
+        float mx = kNegInf;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float mt_ = mx * cl;
+        const bool need = mt_ > m_run + kRescaleSlack;
+        if (__ballot(need)) {
+            const float mnew = need ? mt_ : m_run;
+            const float alpha = (m_run == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(m_run - mnew);
+#pragma unroll
+            for (int mt = 0; mt < NDT; ++mt) o[mt] *= alpha;
+            l_run *= alpha;
+            m_run = mnew;
+        }
+        const float msub = m_run == kNegInf ? 0.f : m_run;
+        f16x8 pb[4];
+        const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt) {
+#pragma unroll
+            for (int sh = 0; sh < 2; ++sh) {
+#pragma unroll
+                for (int e = 0; e < 8; e += 2) {
+                    const int r = 8 * sh + e;
+                    const float x0 = tt ? s1[r] : s0[r];
+                    const float x1 = tt ? s1[r + 1] : s0[r + 1];
+                    const float p0 = __builtin_amdgcn_exp2f(fmaf(x0, cl, -msub));
+                    const float p1 = __builtin_amdgcn_exp2f(fmaf(x1, cl, -msub));
+                    const f16x2 pp = {(_Float16)p0, (_Float16)p1};
+                    l_run = __builtin_amdgcn_fdot2(pp, ones, l_run, false);
+                    pb[2 * tt + sh][e] = pp[0];
+                    pb[2 * tt + sh][e + 1] = pp[1];
+                }
+            }
+        }
+
+        // ---- O^T += V^T P^T
+#pragma unroll
+        for (int mt = 0; mt < NDT; ++mt) {
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                const f16x8 av = *reinterpret_cast<const f16x8*>(Vb + (32 * mt + r32) * VS + 16 * kk + 8 * hh);
+                o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, pb[kk], o[mt], 0, 0, 0);
+            }
+        }
+
+        if (more) stash(buf ^ 1);
+        __syncthreads();
+    }
+
+    // ---- epilogue: O = O^T / l, bf16
+    const float lt = l_run + __shfl_xor(l_run, 32);
+    const float inv = lt > 0.f ? 1.0f / lt : 0.f;
+    const int row = qi * BQ + wave * 32 + r32;
+    if (row < a.N) {
+        uint16_t* op = a.out + ((size_t)bh * a.N + row) * D;
+#pragma unroll
+        for (int mt = 0; mt < NDT; ++mt) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int d0 = 32 * mt + 8 * i + 4 * hh;
+                uint32_t w0 = (uint32_t)f32_to_bf16_bits(o[mt][4 * i + 0] * inv) |
+                              ((uint32_t)f32_to_bf16_bits(o[mt][4 * i + 1] * inv) << 16);
+                uint32_t w1 = (uint32_t)f32_to_bf16_bits(o[mt][4 * i + 2] * inv) |
+                              ((uint32_t)f32_to_bf16_bits(o[mt][4 * i + 3] * inv) << 16);
+                *reinterpret_cast<uint2*>(op + d0) = make_uint2(w0, w1);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Routed attention with f32 inputs (correctness-first path, VALU only).  One thread per
+// query row; K/V (or pooled Kbar/Vbar for correction tiles) staged in LDS one tile at a
+// time; per-key streaming softmax in natural-exp units.
+// ---------------------------------------------------------------------------
+struct AttnArgsF32 {
+    const float* q;
+    const float* k;
+    const float* v;
+    const float* qbar;
+    const float* kbar;
+    const float* vbar;
+    const float* tau;
+    float* out;
+    uint32_t* blkcount;
+    uint32_t* mask_out;
+    int BH, N, NQ, NK, NKr, NC, MW;
+    float scale;
+};
+
+template <int D, int BQ, int MODE>
+__global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
+    constexpr int NT = BQ;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    float* ks = reinterpret_cast<float*>(smem);            // [64][D]
+    float* vs = ks + kBlockK * D;                          // [64][D]
+    float* qt = vs + kBlockK * D;                          // [D][BQ]
+    char* rest = reinterpret_cast<char*>(qt + D * BQ);
+    int* scan_scratch = reinterpret_cast<int*>(rest);
+    float* qb_s = reinterpret_cast<float*>(rest + 64);
+    uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64 + 4 * D);
+    int* list = reinterpret_cast<int*>(rest + 64 + 4 * D + 4 * ((a.MW + 3) & ~3));
+
+    const int bh = blockIdx.y, qi = blockIdx.x, tid = threadIdx.x;
+    int ntiles, nsel;
+    if (MODE == kDense) {
+        ntiles = a.NK;
+        nsel = a.NKr;
+    } else {
+        ntiles = route_and_list<D, NT, MODE>(a.qbar + ((size_t)bh * a.NQ + qi) * D, a.kbar + (size_t)bh * a.NK * D,
+                                             a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, qb_s,
+                                             selw, list, scan_scratch, &nsel);
+        if (a.mask_out)
+            for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
+    }
+    if (tid == 0) a.blkcount[(size_t)bh * a.NQ + qi] = (uint32_t)nsel;
+
+    const int row = qi * BQ + tid;
+    for (int e = tid; e < BQ * D; e += NT) {
+        const int rr = e / D, c = e % D, gr = qi * BQ + rr;
+        qt[c * BQ + rr] = gr < a.N ? a.q[((size_t)bh * a.N + gr) * D + c] : 0.f;
+    }
+    float o[D];
+#pragma unroll
+    for (int c = 0; c < D; ++c) o[c] = 0.f;
+    float m = kNegInf, l = 0.f;
+
+    for (int n = 0; n < ntiles; ++n) {
+        const int code = MODE == kDense ? n : list[n];
+        const bool apx = code & kApxFlag;
+        const int c = code & ~kApxFlag;
+        __syncthreads();
+        for (int e = tid; e < kBlockK * D; e += NT) {
+            const int rr = e / D, cc = e % D;
+            float kv = 0.f, vv = 0.f;
+            if (apx) {
+                const int j = c * kChunk + rr;
+                if (j < a.NKr) {
+                    kv = a.kbar[((size_t)bh * a.NK + j) * D + cc];
+                    vv = a.vbar[((size_t)bh * a.NK + j) * D + cc];
+                }
+            } else {
+                const int gr = c * kBlockK + rr;
+                if (gr < a.N) {
+                    kv = a.k[((size_t)bh * a.N + gr) * D + cc];
+                    vv = a.v[((size_t)bh * a.N + gr) * D + cc];
+                }
+            }
+            ks[e] = kv;
+            vs[e] = vv;
+        }
+        __syncthreads();
+        for (int u = 0; u < kBlockK; ++u) {
+            float bias = 0.f;
+            if (apx) {
+                const int j = c * kChunk + u;
+                if (j >= a.NKr || ((selw[j >> 5] >> (j & 31)) & 1u)) continue;
+                bias = logf((float)min(kBlockK, a.N - j * kBlockK));
+            } else if (c * kBlockK + u >= a.N) {
+                continue;
+            }
+            float dot = 0.f;
+#pragma unroll 16
+            for (int cc = 0; cc < D; ++cc) dot = fmaf(qt[cc * BQ + tid], ks[u * D + cc], dot);
+            const float s = dot * a.scale + bias;
+            if (s > m) {
+                const float alpha = m == kNegInf ? 0.f : expf(m - s);
+                l *= alpha;
+#pragma unroll
+                for (int cc = 0; cc < D; ++cc) o[cc] *= alpha;
+                m = s;
+            }
+            const float p = expf(s - m);
+            l += p;
+#pragma unroll
+            for (int cc = 0; cc < D; ++cc) o[cc] = fmaf(p, vs[u * D + cc], o[cc]);
+        }
+    }
+    if (row < a.N) {
+        const float inv = l > 0.f ? 1.0f / l : 0.f;
+        float* op = a.out + ((size_t)bh * a.N + row) * D;
+#pragma unroll
+        for (int cc = 0; cc < D; ++cc) op[cc] = o[cc] * inv;
+    }
+}
+
+__global__ __launch_bounds__(256) void count_reduce_kernel(const uint32_t* __restrict__ blk, uint32_t* __restrict__ counts,
+                                                           int NQ) {
+    __shared__ uint32_t red[4];
+    const int bh = blockIdx.x, t = threadIdx.x;
+    uint32_t s = 0;
+    for (int i = t; i < NQ; i += 256) s += blk[(size_t)bh * NQ + i];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+    if ((t & 63) == 0) red[t >> 6] = s;
+    __syncthreads();
+    if (t == 0) counts[bh] = red[0] + red[1] + red[2] + red[3];
+}
+
+template <typename K>
+hipError_t allow_lds(K kernel, size_t bytes) {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)bytes);
+}
+
+template <int D, int BQ, int MODE>
+hipError_t launch_attn_bf16(const Shape& s, const AttnArgs& a, hipStream_t st) {
+    const size_t lds = attn_lds_bytes(s);
+    auto kern = routed_attn_kernel<D, BQ, MODE>;
+    hipError_t e = allow_lds(kern, lds);
+    if (e != hipSuccess) return e;
+    const int grid = 8 * a.per_x * a.BH;
+    kern<<<dim3(grid), dim3(BQ * 2), lds, st>>>(a);
+    return hipGetLastError();
+}
+
+template <int D, int BQ, int MODE>
+hipError_t launch_attn_f32(const Shape& s, const AttnArgsF32& a, hipStream_t st) {
+    const size_t lds = attn_lds_bytes(s);
+    auto kern = routed_attn_f32_kernel<D, BQ, MODE>;
+    hipError_t e = allow_lds(kern, lds);
+    if (e != hipSuccess) return e;
+    kern<<<dim3(a.NQ, a.BH), dim3(BQ), lds, st>>>(a);
+    return hipGetLastError();
+}
+
+template <int D, int BQ>
+hipError_t dispatch_bf16_mode(const Shape& s, const AttnArgs& a, hipStream_t st) {
+    switch (s.mode) {
+        case kDense: return launch_attn_bf16<D, BQ, kDense>(s, a, st);
+        case kSparse: return launch_attn_bf16<D, BQ, kSparse>(s, a, st);
+        default: return launch_attn_bf16<D, BQ, kSparseNoCorr>(s, a, st);
+    }
+}
+
+template <int D, int BQ>
+hipError_t dispatch_f32_mode(const Shape& s, const AttnArgsF32& a, hipStream_t st) {
+    switch (s.mode) {
+        case kDense: return launch_attn_f32<D, BQ, kDense>(s, a, st);
+        case kSparse: return launch_attn_f32<D, BQ, kSparse>(s, a, st);
+        default: return launch_attn_f32<D, BQ, kSparseNoCorr>(s, a, st);
+    }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Host-side launch helpers
+// ---------------------------------------------------------------------------
+Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype, int keep_tail_tokens) {
+    Shape s{};
+    s.B = B; s.H = H; s.N = N; s.d = d; s.bq = bq; s.bk = bk;
+    s.mode = mode; s.dtype = dtype;
+    s.forced = bk > 0 ? keep_tail_tokens / bk : 0;
+    s.BH = B * H;
+    s.NQ = bq > 0 ? (N + bq - 1) / bq : 0;
+    s.NK = bk > 0 ? (N + bk - 1) / bk : 0;
+    s.NKr = s.NK - s.forced;
+    s.NC = (s.NKr + kChunk - 1) / kChunk;
+    s.Npad = s.NK * kBlockK;
+    s.MW = (s.NKr + 31) / 32;
+    return s;
+}
+
+size_t attn_lds_bytes(const Shape& s) {
+    const size_t rest = 64 + 4 * (size_t)s.d + 4 * (size_t)((s.MW + 3) & ~3) + 4 * (size_t)(s.NK + s.NC);
+    if (s.dtype == kBF16) {
+        const size_t stage = (size_t)kBlockK * (s.d + 8) * 2 + (size_t)s.d * (kBlockK + 8) * 2;
+        return 2 * stage + rest;
+    }
+    return (size_t)2 * kBlockK * s.d * 4 + (size_t)s.d * s.bq * 4 + rest;
+}
+
+size_t workspace_layout(const Shape& s, char* base, Workspace* ws) {
+    size_t off = 0;
+    auto take = [&](size_t bytes) -> char* {
+        char* p = base ? base + off : nullptr;
+        off += (bytes + 255) & ~(size_t)255;
+        return p;
+    };
+    const size_t BH = s.BH, d = s.d;
+    const bool routing = s.mode != kDense;
+    Workspace w;
+    if (routing) {
+        w.qbar = reinterpret_cast<float*>(take(BH * s.NQ * d * 4));
+        w.kbar = reinterpret_cast<float*>(take(BH * s.NK * d * 4));
+        w.muk = reinterpret_cast<float*>(take(BH * d * 4));
+        w.cov = reinterpret_cast<float*>(take(BH * d * d * 4));
+        w.tau = reinterpret_cast<float*>(take(BH * s.NQ * 4));
+    }
+    if (s.dtype == kBF16) {
+        w.vt = reinterpret_cast<_Float16*>(take(BH * d * (size_t)s.Npad * 2));
+        if (routing) {
+            w.kbar16 = reinterpret_cast<uint16_t*>(take(BH * (size_t)s.NC * kChunk * d * 2));
+            w.vbart = reinterpret_cast<_Float16*>(take(BH * (size_t)s.NC * d * kChunk * 2));
+        }
+    } else if (s.mode == kSparse) {
+        w.vbar = reinterpret_cast<float*>(take(BH * s.NK * d * 4));
+    }
+    w.blkcount = reinterpret_cast<uint32_t*>(take(BH * s.NQ * 4));
+    if (ws) *ws = w;
+    return off;
+}
+
+hipError_t launch_pool_mean(const void* x, float* mean, int dtype, int BH, int N, int d, int blk, hipStream_t st) {
+    const int nb = (N + blk - 1) / blk;
+    if (dtype == kBF16)
+        pool_mean_kernel<uint16_t><<<dim3(nb, BH), dim3(256), 0, st>>>(static_cast<const uint16_t*>(x), mean, N, d, blk, nb);
+    else
+        pool_mean_kernel<float><<<dim3(nb, BH), dim3(256), 0, st>>>(static_cast<const float*>(x), mean, N, d, blk, nb);
+    return hipGetLastError();
+}
+
+hipError_t launch_moments(const float* kbar, float* muk, float* cov, int BH, int NK, int NKr, int d, hipStream_t st) {
+    if (d == 128) moments_kernel<128><<<dim3(128 / 16, BH), dim3(256), 0, st>>>(kbar, muk, cov, NK, NKr);
+    else moments_kernel<64><<<dim3(64 / 16, BH), dim3(256), 0, st>>>(kbar, muk, cov, NK, NKr);
+    return hipGetLastError();
+}
+
+hipError_t launch_tau(const float* qbar, const float* muk, const float* cov, float* tau, float* mu, float* sigma,
+                      int BH, int NQ, int d, float beta, hipStream_t st) {
+    const float scale = 1.0f / sqrtf((float)d);
+    const size_t lds = ((size_t)d * d + 16 * d + d + 8) * 4;
+    const dim3 grid((NQ + 15) / 16, BH);
+    if (d == 128) {
+        hipError_t e = allow_lds(tau_kernel<128>, lds);
+        if (e != hipSuccess) return e;
+        tau_kernel<128><<<grid, dim3(256), lds, st>>>(qbar, muk, cov, tau, mu, sigma, NQ, beta, scale);
+    } else {
+        hipError_t e = allow_lds(tau_kernel<64>, lds);
+        if (e != hipSuccess) return e;
+        tau_kernel<64><<<grid, dim3(256), lds, st>>>(qbar, muk, cov, tau, mu, sigma, NQ, beta, scale);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_forward(const Shape& s, const void* q, const void* k, const void* v, void* out, float beta,
+                          const Workspace& ws, uint32_t* counts, uint32_t* mask_out, hipStream_t st,
+                          hipEvent_t ev_start, hipEvent_t ev_stop) {
+    const bool routing = s.mode != kDense;
+    const int d = s.d;
+    hipError_t e;
+    const float scale = 1.0f / sqrtf((float)d);
+    if (s.dtype == kBF16) {
+        if (routing) {
+            e = launch_pool_mean(q, ws.qbar, kBF16, s.BH, s.N, d, s.bq, st);
+            if (e != hipSuccess) return e;
+        }
+        const int nj = routing ? (s.NC * kChunk > s.NK ? s.NC * kChunk : s.NK) : s.NK;
+        const uint16_t* kk = static_cast<const uint16_t*>(k);
+        const uint16_t* vv = static_cast<const uint16_t*>(v);
+        if (d == 128)
+            prep_kv_kernel<128><<<dim3(nj, s.BH), dim3(256), 0, st>>>(kk, vv, ws.kbar, ws.kbar16, ws.vbart, ws.vt, s.N,
+                                                                      s.NK, s.NKr, s.NC, s.Npad, routing ? 1 : 0);
+        else
+            prep_kv_kernel<64><<<dim3(nj, s.BH), dim3(256), 0, st>>>(kk, vv, ws.kbar, ws.kbar16, ws.vbart, ws.vt, s.N,
+                                                                     s.NK, s.NKr, s.NC, s.Npad, routing ? 1 : 0);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (routing) {
+            if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, s.BH, s.NK, s.NKr, d, st)) != hipSuccess) return e;
+            if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, st)) != hipSuccess)
+                return e;
+        }
+        AttnArgs a{};
+        a.q = static_cast<const uint16_t*>(q);
+        a.k = kk;
+        a.vt = ws.vt;
+        a.qbar = ws.qbar;
+        a.kbar = ws.kbar;
+        a.kbar16 = ws.kbar16;
+        a.vbart = ws.vbart;
+        a.tau = ws.tau;
+        a.out = static_cast<uint16_t*>(out);
+        a.blkcount = ws.blkcount;
+        a.mask_out = mask_out;
+        a.BH = s.BH; a.N = s.N; a.NQ = s.NQ; a.NK = s.NK; a.NKr = s.NKr; a.Npad = s.Npad; a.NC = s.NC; a.MW = s.MW;
+        a.per_x = (s.NQ + 7) / 8;
+        a.scale = scale;
+        a.c_log2 = scale * kLog2e;
+        if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
+        if (d == 128) e = s.bq == 128 ? dispatch_bf16_mode<128, 128>(s, a, st) : dispatch_bf16_mode<128, 64>(s, a, st);
+        else e = s.bq == 128 ? dispatch_bf16_mode<64, 128>(s, a, st) : dispatch_bf16_mode<64, 64>(s, a, st);
+        if (e != hipSuccess) return e;
+        if (ev_stop && (e = hipEventRecord(ev_stop, st)) != hipSuccess) return e;
+    } else {
+        if (routing) {
+            if ((e = launch_pool_mean(q, ws.qbar, kF32, s.BH, s.N, d, s.bq, st)) != hipSuccess) return e;
+            if ((e = launch_pool_mean(k, ws.kbar, kF32, s.BH, s.N, d, s.bk, st)) != hipSuccess) return e;
+            if (s.mode == kSparse && (e = launch_pool_mean(v, ws.vbar, kF32, s.BH, s.N, d, s.bk, st)) != hipSuccess)
+                return e;
+            if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, s.BH, s.NK, s.NKr, d, st)) != hipSuccess) return e;
+            if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, st)) != hipSuccess)
+                return e;
+        }
+        AttnArgsF32 a{};
+        a.q = static_cast<const float*>(q);
+        a.k = static_cast<const float*>(k);
+        a.v = static_cast<const float*>(v);
+        a.qbar = ws.qbar;
+        a.kbar = ws.kbar;
+        a.vbar = ws.vbar;
+        a.tau = ws.tau;
+        a.out = static_cast<float*>(out);
+        a.blkcount = ws.blkcount;
+        a.mask_out = mask_out;
+        a.BH = s.BH; a.N = s.N; a.NQ = s.NQ; a.NK = s.NK; a.NKr = s.NKr; a.NC = s.NC; a.MW = s.MW;
+        a.scale = scale;
+        if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
+        if (d == 128) e = s.bq == 128 ? dispatch_f32_mode<128, 128>(s, a, st) : dispatch_f32_mode<128, 64>(s, a, st);
+        else e = s.bq == 128 ? dispatch_f32_mode<64, 128>(s, a, st) : dispatch_f32_mode<64, 64>(s, a, st);
+        if (e != hipSuccess) return e;
+        if (ev_stop && (e = hipEventRecord(ev_stop, st)) != hipSuccess) return e;
+    }
+    count_reduce_kernel<<<dim3(s.BH), dim3(256), 0, st>>>(ws.blkcount, counts, s.NQ);
+    return hipGetLastError();
+}
+
+}  // namespace sol

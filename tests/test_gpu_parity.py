@@ -1,0 +1,197 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 CPU oracle.
+
+Small shapes are compared element by element over every output; the full
+workload shapes (in the launch configuration the benchmark times) are compared on
+the complete selection mask and on sampled query blocks of sampled heads.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import sol_attn_oracle as ora
+from paper_2607_24027_amd import binding as sb
+from paper_2607_24027_amd import configs, synth
+from tests.parity import (assert_mask_matches, assert_output_close, small_workload, to_np)
+
+pytestmark = pytest.mark.gpu
+
+INF = math.inf
+
+
+@pytest.fixture(scope="module")
+def dev():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    sb.lib()  # fail loudly if the library is missing
+    return torch.device("cuda:0")
+
+
+SMALL = {
+    # name: (grid, d, block_q, dtype, text tokens)
+    "bf16_d128_q128": ((5, 10, 100), 128, 128, "bf16", 0),     # N=5000: NQ=40 (tail 8), NK=79 (tail 8), 2 chunks
+    "bf16_d64_q64_text": ((4, 20, 64), 64, 64, "bf16", 512),   # N=5632: 8 forced text blocks
+    "bf16_d128_q64_text": ((60, 70), 128, 64, "bf16", 576),    # 2D grid, N=4776: ragged text tail
+    "f32_d64_q64": ((4, 16, 32), 64, 64, "f32", 0),            # the tiny workload shape
+    "f32_d128_q128": ((3, 10, 41), 128, 128, "f32", 0),        # N=1230, ragged
+}
+_cache = {}
+
+
+def small_inputs(name):
+    if name not in _cache:
+        grid, d, bq, dtype, text = SMALL[name]
+        w = small_workload(name, grid, d, bq, dtype=dtype, text_tokens=text)
+        _cache[name] = (w, synth.make_qkv(w))
+    return _cache[name]
+
+
+def run_gpu(dev, w, q, k, v, beta, mode, want_mask=True):
+    qd, kd, vd = (t.to(dev) for t in (q, k, v))
+    nkr = w.NK - w.text_tokens // 64
+    mw = sb.mask_words(nkr)
+    mask = torch.zeros((w.B, w.H, w.NQ, mw), dtype=torch.int32, device=dev) if want_mask else None
+    counts = torch.full((w.B, w.H), -1, dtype=torch.int32, device=dev)
+    out = sb.forward(qd, kd, vd, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens,
+                     counts=counts, mask_out=mask)
+    torch.cuda.synchronize()
+    gmask = None
+    if want_mask and mode != "dense":
+        gmask = sb.unpack_mask(mask.cpu().numpy().view(np.uint32), nkr)
+    return out, gmask, counts.cpu().numpy().view(np.uint32)
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+@pytest.mark.parametrize("mode,beta", [("dense", 0.0), ("sparse", 0.8), ("sparse", -INF), ("sparse", INF),
+                                       ("sparse_no_correction", 0.8), ("sparse_no_correction", -INF),
+                                       ("sparse_no_correction", INF), ("sparse", 0.0)])
+def test_forward_parity_small(dev, name, mode, beta):
+    w, (q, k, v) = small_inputs(name)
+    print(f"[parity] {name} mode={mode} beta={beta}", flush=True)
+    out, gmask, counts = run_gpu(dev, w, q, k, v, beta, mode)
+    qn, kn, vn = to_np(q), to_np(k), to_np(v)
+    ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens)
+    if mode != "dense":
+        flips = assert_mask_matches(gmask, ref["mask"], ref["s_hat"], ref["tau"])
+        if flips:
+            ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens, mask=gmask)
+        assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
+    else:
+        nkr = w.NK - w.text_tokens // 64
+        assert np.all(counts == w.NQ * nkr)
+    assert_output_close(to_np(out), ref["out"], w.dtype, f"{name}/{mode}/{beta}")
+
+
+@pytest.mark.parametrize("name", ["bf16_d128_q128", "f32_d64_q64", "bf16_d64_q64_text"])
+def test_pool_blocks_parity(dev, name):
+    w, (q, k, v) = small_inputs(name)
+    qbar, kbar, vbar = sb.pool_blocks(q.to(dev), k.to(dev), v.to(dev), w.block_q, 64)
+    torch.cuda.synchronize()
+    for got, x, blk in ((qbar, q, w.block_q), (kbar, k, 64), (vbar, v, 64)):
+        want, _ = ora.pool_means(to_np(x), blk)
+        np.testing.assert_allclose(to_np(got), want, rtol=1e-5, atol=2e-6)
+
+
+@pytest.mark.parametrize("name", ["bf16_d128_q128", "f32_d64_q64"])
+@pytest.mark.parametrize("beta", [0.8, -0.5, -INF, INF])
+def test_thresholds_parity(dev, name, beta):
+    w, (q, k, v) = small_inputs(name)
+    qbar, kbar, _ = sb.pool_blocks(q.to(dev), k.to(dev), v.to(dev), w.block_q, 64)
+    tau, mu, sigma = sb.thresholds(qbar, kbar, beta)
+    torch.cuda.synchronize()
+    scale = 1 / math.sqrt(w.d)
+    s_hat = ora.proxy_scores(to_np(qbar), to_np(kbar), scale)
+    mu_r, sd_r = ora.row_stats(s_hat)
+    np.testing.assert_allclose(to_np(mu), mu_r, atol=1e-5, rtol=1e-5)
+    np.testing.assert_allclose(to_np(sigma), sd_r, atol=1e-5, rtol=1e-5)
+    tau_r = ora.thresholds(mu_r, sd_r, beta)
+    if math.isinf(beta):
+        assert np.array_equal(to_np(tau), tau_r)
+    else:
+        np.testing.assert_allclose(to_np(tau), tau_r, atol=1e-5, rtol=1e-5)
+
+
+def test_beta_minus_inf_is_bitwise_dense(dev):
+    w, (q, k, v) = small_inputs("bf16_d128_q128")
+    dense, _, _ = run_gpu(dev, w, q, k, v, 0.0, "dense", want_mask=False)
+    for mode in ("sparse", "sparse_no_correction"):
+        out, gmask, counts = run_gpu(dev, w, q, k, v, -INF, mode)
+        assert gmask.all()
+        assert torch.equal(out, dense)
+
+
+def test_no_correction_with_nothing_selected_is_zero(dev):
+    w, (q, k, v) = small_inputs("bf16_d128_q128")
+    out, gmask, counts = run_gpu(dev, w, q, k, v, INF, "sparse_no_correction")
+    assert not gmask.any() and not counts.any()
+    assert torch.count_nonzero(out) == 0
+
+
+def test_short_form_and_stats(dev):
+    w, (q, k, v) = small_inputs("bf16_d128_q128")
+    qd, kd, vd = (t.to(dev) for t in (q, k, v))
+    ref, gmask, counts = run_gpu(dev, w, q, k, v, 0.8, "sparse")
+    out = torch.empty_like(qd)
+    sb.forward_short(qd, kd, vd, out, w.block_q, 64, 0.8, "sparse")
+    frac = sb.stats(w.B, w.H)
+    assert torch.equal(out, ref)
+    nkr = w.NK
+    np.testing.assert_allclose(frac, (gmask.sum(axis=(2, 3)) / (w.NQ * nkr)).ravel(), rtol=1e-6)
+
+
+def test_caller_workspace(dev):
+    w, (q, k, v) = small_inputs("bf16_d64_q64_text")
+    qd, kd, vd = (t.to(dev) for t in (q, k, v))
+    ref = sb.forward(qd, kd, vd, w.block_q, 64, 0.8, "sparse", keep_tail_tokens=w.text_tokens)
+    nbytes = sb.workspace_bytes(w.B, w.H, w.N, w.d, w.block_q, 64, "sparse", sb.SOL_BF16, w.text_tokens)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    out = sb.forward(qd, kd, vd, w.block_q, 64, 0.8, "sparse", keep_tail_tokens=w.text_tokens, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
+    with pytest.raises(sb.SolAttnError) as ei:
+        sb.forward(qd, kd, vd, w.block_q, 64, 0.8, "sparse", keep_tail_tokens=w.text_tokens, workspace=ws[: nbytes // 2])
+    assert ei.value.code == sb.SOL_ERR_WORKSPACE
+
+
+def test_deterministic(dev):
+    w, (q, k, v) = small_inputs("bf16_d128_q128")
+    a, _, _ = run_gpu(dev, w, q, k, v, 0.8, "sparse")
+    b, _, _ = run_gpu(dev, w, q, k, v, 0.8, "sparse")
+    assert torch.equal(a, b)
+
+
+# --------------------------------------------------------------------------- full workload shapes
+
+@pytest.fixture(scope="module", params=["video480p", "image", "video720p"])
+def full(request, dev):
+    w = configs.WORKLOADS[request.param]
+    print(f"[parity] generating {w.name}", flush=True)
+    q, k, v = synth.make_qkv(w, workers=synth.default_workers())
+    beta = configs.beta_for(w)
+    print(f"[parity] oracle routing {w.name}", flush=True)
+    r = ora.routing(q.float().numpy(), k.float().numpy(), w.block_q, 64, beta, keep_tail_tokens=w.text_tokens)
+    yield w, (q, k, v), beta, r
+    del q, k, v, r
+
+
+@pytest.mark.parametrize("mode", ["sparse", "sparse_no_correction", "dense"])
+def test_full_size_sampled(dev, full, mode):
+    w, (q, k, v), beta, r = full
+    print(f"[parity] full {w.name} mode={mode}", flush=True)
+    out, gmask, counts = run_gpu(dev, w, q, k, v, beta, mode)
+    heads = [(0, 0), (w.B - 1, w.H - 1)]
+    qblocks = sorted({0, 1, w.NQ // 2, w.NQ - 1})
+    mask_for_oracle = None
+    if mode != "dense":
+        flips = assert_mask_matches(gmask, r["mask"], r["s_hat"], r["tau"])
+        print(f"[parity] {w.name}: {flips} in-band mask flips of {gmask.size}", flush=True)
+        assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
+        mask_for_oracle = gmask
+    qs, ks, vs = (x[[b for b, _ in heads], [h for _, h in heads]].float().numpy()[None] for x in (q, k, v))
+    # oracle on the two sampled heads, packed as a [1, 2, N, d] problem
+    sub_mask = None if mask_for_oracle is None else mask_for_oracle[[b for b, _ in heads], [h for _, h in heads]][None]
+    ref = ora.forward(qs, ks, vs, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens,
+                      query_blocks=qblocks, mask=sub_mask)
+    got = out[[b for b, _ in heads], [h for _, h in heads]].float().cpu().numpy()[None].astype(np.float64)
+    rows = np.concatenate([np.arange(i * w.block_q, min((i + 1) * w.block_q, w.N)) for i in qblocks])
+    assert_output_close(got[:, :, rows], ref["out"][:, :, rows], w.dtype, f"{w.name}/{mode}")
