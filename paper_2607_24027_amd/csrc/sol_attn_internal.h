@@ -30,7 +30,7 @@ struct Workspace {
     float* qbar = nullptr;       // [BH][NQ][d]
     float* kbar = nullptr;       // [BH][NK][d]
     float* vbar = nullptr;       // [BH][NK][d]            (f32 path)
-    uint16_t* kbar16 = nullptr;  // [BH][NC*64][d] bf16     (bf16 sparse)
+    _Float16* kbarh = nullptr;   // [BH][NC*64][d] f16      (bf16 routing modes)
     _Float16* vbart = nullptr;   // [BH][NC][d][64] f16     (bf16 sparse)
     _Float16* vt = nullptr;      // [BH][d][Npad] f16       (bf16)
     float* muk = nullptr;        // [BH][d]

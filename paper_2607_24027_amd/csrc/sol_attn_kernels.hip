@@ -2,7 +2,7 @@
 //
 // Pipeline of one forward (bf16 inputs):
 //   1. pool_mean      Qbar_i = token mean of query block i           (Eq. block_proxy)
-//   2. prep_kv        Kbar_j (f32 + bf16 copy), Vbar_j (f16, correction layout) and the
+//   2. prep_kv        Kbar_j (f32 + f16 copy), Vbar_j (f16, correction layout) and the
 //                     f16 transposed V used by the exact tiles
 //   3. moments        mean and centred covariance of the routable pooled keys, f64 sums
 //   4. tau            tau_i = mu_i + beta*sigma_i from the moments   (Eqs. threshold_routing,
@@ -119,7 +119,7 @@ __global__ __launch_bounds__(256) void pool_mean_kernel(const T* __restrict__ x,
 //          past N are zero.
 //   routing modes additionally:
 //   kbar   [BH][NK][D] f32 means (routing proxies and moments)
-//   kbar16 [BH][NC*64][D] bf16 means of routable blocks (A operand of correction tiles);
+//   kbarh  [BH][NC*64][D] f16 means of routable blocks (A operand of correction tiles);
 //          zero for forced and padding rows
 //   vbart  [BH][NC][D][64] f16 value means in correction layout (slot swap23(j%64));
 //          zero for forced and padding slots
@@ -127,7 +127,7 @@ __global__ __launch_bounds__(256) void pool_mean_kernel(const T* __restrict__ x,
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
-                                                      float* __restrict__ kbar, uint16_t* __restrict__ kbar16,
+                                                      float* __restrict__ kbar, _Float16* __restrict__ kbarh,
                                                       _Float16* __restrict__ vbart, _Float16* __restrict__ vt,
                                                       int N, int NK, int NKr, int NC, int Npad, int routing) {
     constexpr int CPR = D / 8;          // 16-byte chunks per row
@@ -140,7 +140,7 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict
 
     if (j >= NK) {  // padding rows of the last correction tile
         for (int c = t; c < D; c += 256) {
-            kbar16[((size_t)bh * NC * kChunk + j) * D + c] = 0;
+            kbarh[((size_t)bh * NC * kChunk + j) * D + c] = (_Float16)0.f;
             vbart[(((size_t)bh * NC + j / kChunk) * D + c) * kChunk + swap23(j % kChunk)] = (_Float16)0.f;
         }
         return;
@@ -222,7 +222,7 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict
         const float m = s * inv;
         kbar[((size_t)bh * NK + j) * D + t] = m;
         if (j < NC * kChunk)
-            kbar16[((size_t)bh * NC * kChunk + j) * D + t] = j < NKr ? f32_to_bf16_bits(m) : (uint16_t)0;
+            kbarh[((size_t)bh * NC * kChunk + j) * D + t] = j < NKr ? (_Float16)m : (_Float16)0.f;
     }
 }
 
@@ -450,7 +450,7 @@ struct AttnArgs {
     const _Float16* vt;
     const float* qbar;
     const float* kbar;
-    const uint16_t* kbar16;
+    const _Float16* kbarh;
     const _Float16* vbart;
     const float* tau;
     uint16_t* out;
@@ -539,7 +539,7 @@ __global__ __launch_bounds__(BQ * 2) void routed_attn_kernel(AttnArgs a) {
         size_t vstride;
         if (code & kApxFlag) {
             const int c = code & ~kApxFlag;
-            kp = a.kbar16 + ((size_t)bh * a.NC * kChunk + (size_t)c * kChunk) * D;
+            kp = reinterpret_cast<const uint16_t*>(a.kbarh) + ((size_t)bh * a.NC * kChunk + (size_t)c * kChunk) * D;
             vp = a.vbart + ((size_t)bh * a.NC + c) * D * kChunk;
             nrows = kChunk;
             vstride = kChunk;
@@ -589,14 +589,29 @@ __global__ __launch_bounds__(BQ * 2) void routed_attn_kernel(AttnArgs a) {
         const uint16_t* Kb = kbuf(buf);
         const _Float16* Vb = vbuf(buf);
 
-        // ---- S^T = K Q^T  (two 32-key M-tiles)
+        // ---- S^T = K Q^T  (two 32-key M-tiles).  Exact tiles: bf16 keys and queries.
+        // Correction tiles: f16 pooled keys against an f16 copy of the queries (exact for
+        // bf16 values in the f16 range), so the pooled keys keep 11 significant bits.
         f32x16 s0 = f32x16{}, s1 = f32x16{};
+        if (code & kApxFlag) {
 #pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-            const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(Kb + r32 * KS + 16 * ks + 8 * hh);
-            const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(Kb + (32 + r32) * KS + 16 * ks + 8 * hh);
-            s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[ks], s0, 0, 0, 0);
-            s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[ks], s1, 0, 0, 0);
+            for (int ks = 0; ks < NKS; ++ks) {
+                f16x8 qh;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) qh[e] = (_Float16)(float)qf[ks][e];
+                const f16x8 a0 = *reinterpret_cast<const f16x8*>(Kb + r32 * KS + 16 * ks + 8 * hh);
+                const f16x8 a1 = *reinterpret_cast<const f16x8*>(Kb + (32 + r32) * KS + 16 * ks + 8 * hh);
+                s0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a0, qh, s0, 0, 0, 0);
+                s1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a1, qh, s1, 0, 0, 0);
+            }
+        } else {
+#pragma unroll
+            for (int ks = 0; ks < NKS; ++ks) {
+                const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(Kb + r32 * KS + 16 * ks + 8 * hh);
+                const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(Kb + (32 + r32) * KS + 16 * ks + 8 * hh);
+                s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[ks], s0, 0, 0, 0);
+                s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[ks], s1, 0, 0, 0);
+            }
         }
 
         // ---- masks: ragged last key block, or correction-tile multiplicity / exclusion
@@ -921,7 +936,7 @@ size_t workspace_layout(const Shape& s, char* base, Workspace* ws) {
     if (s.dtype == kBF16) {
         w.vt = reinterpret_cast<_Float16*>(take(BH * d * (size_t)s.Npad * 2));
         if (routing) {
-            w.kbar16 = reinterpret_cast<uint16_t*>(take(BH * (size_t)s.NC * kChunk * d * 2));
+            w.kbarh = reinterpret_cast<_Float16*>(take(BH * (size_t)s.NC * kChunk * d * 2));
             w.vbart = reinterpret_cast<_Float16*>(take(BH * (size_t)s.NC * d * kChunk * 2));
         }
     } else if (s.mode == kSparse) {
@@ -980,10 +995,10 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         const uint16_t* kk = static_cast<const uint16_t*>(k);
         const uint16_t* vv = static_cast<const uint16_t*>(v);
         if (d == 128)
-            prep_kv_kernel<128><<<dim3(nj, s.BH), dim3(256), 0, st>>>(kk, vv, ws.kbar, ws.kbar16, ws.vbart, ws.vt, s.N,
+            prep_kv_kernel<128><<<dim3(nj, s.BH), dim3(256), 0, st>>>(kk, vv, ws.kbar, ws.kbarh, ws.vbart, ws.vt, s.N,
                                                                       s.NK, s.NKr, s.NC, s.Npad, routing ? 1 : 0);
         else
-            prep_kv_kernel<64><<<dim3(nj, s.BH), dim3(256), 0, st>>>(kk, vv, ws.kbar, ws.kbar16, ws.vbart, ws.vt, s.N,
+            prep_kv_kernel<64><<<dim3(nj, s.BH), dim3(256), 0, st>>>(kk, vv, ws.kbar, ws.kbarh, ws.vbart, ws.vt, s.N,
                                                                      s.NK, s.NKr, s.NC, s.Npad, routing ? 1 : 0);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (routing) {
@@ -997,7 +1012,7 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         a.vt = ws.vt;
         a.qbar = ws.qbar;
         a.kbar = ws.kbar;
-        a.kbar16 = ws.kbar16;
+        a.kbarh = ws.kbarh;
         a.vbart = ws.vbart;
         a.tau = ws.tau;
         a.out = static_cast<uint16_t*>(out);
