@@ -22,6 +22,7 @@
 #include "sol_attn_internal.h"
 
 #include <cmath>
+#include <type_traits>
 
 namespace sol {
 namespace {
@@ -345,11 +346,13 @@ __global__ __launch_bounds__(256) void tau_kernel(const float* __restrict__ qbar
 
 // ---------------------------------------------------------------------------
 // Routing prologue shared by both attention kernels: selection bits of every routable key
-// block for query block qi into selw (LDS), then the ordered tile list:
-//   for each chunk c of 64 routable blocks: [correction tile c if it has an unselected
-//   valid block, sparse mode only] + exact tiles of its selected blocks; then forced blocks.
-// Correction tiles are encoded as kApxFlag | c.  Returns the list length; *nsel receives the
-// number of selected routable blocks.
+// block for query block qi into selw (LDS), then the tile list:
+//   [correction tiles: every chunk c of 64 routable blocks with an unselected valid block,
+//    sparse mode only, encoded kApxFlag | c] [selected routable blocks, increasing j]
+//   [forced blocks].
+// The online softmax is order independent, so grouping the correction tiles first changes
+// only the floating-point summation order.  Returns the list length; *napx receives the
+// number of correction tiles and *nsel the number of selected routable blocks.
 // ---------------------------------------------------------------------------
 constexpr int kApxFlag = 1 << 30;
 
@@ -379,7 +382,7 @@ __device__ int block_scan_incl(int v, int* scratch, int* total) {
 template <int D, int NT, int MODE>
 __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __restrict__ kbar_h, float tau_i,
                               float scale, int NKr, int NK, int MW, int NC, float* qb_s, uint32_t* selw,
-                              int* list, int* scan_scratch, int* nsel) {
+                              int* list, int* scan_scratch, int* napx, int* nsel) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int c = tid; c < D; c += NT) qb_s[c] = qbar_i[c];
     __syncthreads();
@@ -407,38 +410,46 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
         }
     }
     __syncthreads();
-    int running = 0, nsel_tot = 0;
+    auto chunk_bits = [&](int c) -> uint64_t {
+        const uint32_t lo = selw[2 * c];
+        const uint32_t hi = (2 * c + 1 < MW) ? selw[2 * c + 1] : 0u;
+        return (uint64_t)lo | ((uint64_t)hi << 32);
+    };
+    // pass 1: correction tiles
+    int n_apx = 0;
+    if (MODE == kSparse) {
+        for (int c0 = 0; c0 < NC; c0 += NT) {
+            const int c = c0 + tid;
+            int apx = 0;
+            if (c < NC) apx = __popcll(chunk_bits(c)) < min(kChunk, NKr - c * kChunk) ? 1 : 0;
+            int tot;
+            const int incl = block_scan_incl<NT>(apx, scan_scratch, &tot);
+            if (apx) list[n_apx + incl - 1] = kApxFlag | c;
+            n_apx += tot;
+        }
+    }
+    // pass 2: selected blocks in increasing order
+    int n_sel = 0;
     for (int c0 = 0; c0 < NC; c0 += NT) {
         const int c = c0 + tid;
-        uint64_t bits = 0;
-        int ns = 0, apx = 0;
-        if (c < NC) {
-            const uint32_t lo = selw[2 * c];
-            const uint32_t hi = (2 * c + 1 < MW) ? selw[2 * c + 1] : 0u;
-            bits = (uint64_t)lo | ((uint64_t)hi << 32);
-            ns = __popcll(bits);
-            const int valid = min(kChunk, NKr - c * kChunk);
-            apx = (MODE == kSparse && ns < valid) ? 1 : 0;
-        }
+        uint64_t bits = c < NC ? chunk_bits(c) : 0ull;
+        const int ns = __popcll(bits);
         int tot;
-        const int packed = (ns + apx) | (ns << 16);
-        const int incl = block_scan_incl<NT>(packed, scan_scratch, &tot);
-        int pos = running + (incl & 0xffff) - (ns + apx);
-        if (c < NC) {
-            if (apx) list[pos++] = kApxFlag | c;
-            while (bits) {
-                const int b = __builtin_ctzll(bits);
-                bits &= bits - 1;
-                list[pos++] = c * kChunk + b;
-            }
+        const int incl = block_scan_incl<NT>(ns, scan_scratch, &tot);
+        int pos = n_apx + n_sel + incl - ns;
+        while (bits) {
+            const int b = __builtin_ctzll(bits);
+            bits &= bits - 1;
+            list[pos++] = c * kChunk + b;
         }
-        running += tot & 0xffff;
-        nsel_tot += tot >> 16;
+        n_sel += tot;
     }
-    for (int j = NKr + tid; j < NK; j += NT) list[running + (j - NKr)] = j;
+    const int n_exact0 = n_apx + n_sel;
+    for (int j = NKr + tid; j < NK; j += NT) list[n_exact0 + (j - NKr)] = j;
     __syncthreads();
-    *nsel = nsel_tot;
-    return running + (NK - NKr);
+    *napx = n_apx;
+    *nsel = n_sel;
+    return n_exact0 + (NK - NKr);
 }
 
 // ---------------------------------------------------------------------------
@@ -458,23 +469,33 @@ struct AttnArgs {
     uint32_t* mask_out;
     int BH, N, NQ, NK, NKr, Npad, NC, MW, per_x;
     float scale, c_log2;
+    float bias_full, bias_last;   // log2(n_j)/c_log2 for full blocks and for the last block
 };
 
+// LDS tiles of the fused kernel, without padding.  A K tile is 64 rows x D bf16 (D/8 16-byte
+// chunks per row), a V^T tile is D rows x 64 f16 (8 chunks per row).  Chunk c of row r is
+// stored at chunk position r*CPR + (c ^ (r mod CPR)), so the 16-byte operand reads of 8
+// consecutive rows hit 8 different bank groups.
 template <int D>
 struct TileLds {
-    static constexpr int KS = D + 8;          // bf16 K row stride (elements): 16-byte pad
-    static constexpr int VS = kBlockK + 8;    // f16 V^T row stride (elements): 16-byte pad
-    static constexpr int KBYTES = kBlockK * KS * 2;
-    static constexpr int VBYTES = D * VS * 2;
+    static constexpr int KCPR = D / 8;
+    static constexpr int VCPR = kBlockK / 8;
+    static constexpr int KBYTES = kBlockK * D * 2;
+    static constexpr int VBYTES = D * kBlockK * 2;
     static constexpr int STAGE = KBYTES + VBYTES;
+    __device__ static int kpos(int r, int c) { return r * KCPR + (c ^ (r & (KCPR - 1))); }
+    __device__ static int vpos(int r, int c) { return r * VCPR + (c ^ (r & (VCPR - 1))); }
 };
 
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
 template <int D, int BQ, int MODE>
-__global__ __launch_bounds__(BQ * 2) void routed_attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void routed_attn_kernel(AttnArgs a) {
     constexpr int NT = BQ * 2;            // 64 threads per 32 query rows
-    constexpr int KCH = kBlockK * D * 2 / 16 / NT;   // 16-byte K chunks per thread
-    constexpr int VCH = D * kBlockK * 2 / 16 / NT;   // 16-byte V^T chunks per thread
-    constexpr int KS = TileLds<D>::KS, VS = TileLds<D>::VS;
+    constexpr int NW = NT / 64;
+    using L = TileLds<D>;
+    constexpr int KPW = L::KBYTES / 1024 / NW;   // direct-to-LDS wave loads per wave (K tile)
+    constexpr int VPW = L::VBYTES / 1024 / NW;   // same for the V^T tile
     constexpr int NDT = D / 32;           // output M-tiles (d rows)
     constexpr int NKS = D / 16;           // k-steps of QK^T
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -490,54 +511,42 @@ __global__ __launch_bounds__(BQ * 2) void routed_attn_kernel(AttnArgs a) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int r32 = lane & 31, hh = lane >> 5;
 
-    auto kbuf = [&](int b) { return reinterpret_cast<uint16_t*>(smem + b * TileLds<D>::STAGE); };
-    auto vbuf = [&](int b) { return reinterpret_cast<_Float16*>(smem + b * TileLds<D>::STAGE + TileLds<D>::KBYTES); };
-    char* rest = smem + 2 * TileLds<D>::STAGE;
+    char* rest = smem + 2 * L::STAGE;
     int* scan_scratch = reinterpret_cast<int*>(rest);
     float* qb_s = reinterpret_cast<float*>(rest + 64);
     uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64 + 4 * D);
     int* list = reinterpret_cast<int*>(rest + 64 + 4 * D + 4 * ((a.MW + 3) & ~3));
 
-    int ntiles, nsel;
+    int ntiles, nsel, napx = 0;
     if (MODE == kDense) {
         ntiles = a.NK;
         nsel = a.NKr;
     } else {
         ntiles = route_and_list<D, NT, MODE>(a.qbar + ((size_t)bh * a.NQ + qi) * D, a.kbar + (size_t)bh * a.NK * D,
                                              a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, qb_s,
-                                             selw, list, scan_scratch, &nsel);
+                                             selw, list, scan_scratch, &napx, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
     if (tid == 0) a.blkcount[(size_t)bh * a.NQ + qi] = (uint32_t)nsel;
 
-    // Q fragment (B operand of S^T = K Q^T): lane holds row r32 of its wave, d-range 8*hh.
-    bf16x8 qf[NKS];
-    {
-        const int row = qi * BQ + wave * 32 + r32;
-        if (row < a.N) {
-            const uint16_t* qp = a.q + ((size_t)bh * a.N + row) * D + 8 * hh;
-#pragma unroll
-            for (int ks = 0; ks < NKS; ++ks) qf[ks] = *reinterpret_cast<const bf16x8*>(qp + 16 * ks);
-        } else {
-#pragma unroll
-            for (int ks = 0; ks < NKS; ++ks) qf[ks] = bf16x8{};
-        }
-    }
+    const int qrow = qi * BQ + wave * 32 + r32;
+    const uint16_t* qrow_p = a.q + ((size_t)bh * a.N + min(qrow, a.N - 1)) * D + 8 * hh;
 
     f32x16 o[NDT];
 #pragma unroll
     for (int mt = 0; mt < NDT; ++mt) o[mt] = f32x16{};
     float m_run = kNegInf, l_run = 0.f;
 
-    u32x4 kr[KCH], vr[VCH];
     auto tile_code = [&](int n) -> int { return MODE == kDense ? n : list[n]; };
-    auto fetch = [&](int code) {
+    // Issue the global->LDS copies of tile `code` into stage `buf`.  Each lane moves one
+    // 16-byte chunk per instruction; rows past the end of the sequence are clamped to the
+    // last valid row (their scores are masked to -inf, their values are zero in V^T).
+    auto issue = [&](int code, int buf) {
         const uint16_t* kp;
         const _Float16* vp;
-        int nrows;
-        size_t vstride;
-        if (code & kApxFlag) {
+        int nrows, vstride;
+        if (MODE != kDense && (code & kApxFlag)) {
             const int c = code & ~kApxFlag;
             kp = reinterpret_cast<const uint16_t*>(a.kbarh) + ((size_t)bh * a.NC * kChunk + (size_t)c * kChunk) * D;
             vp = a.vbart + ((size_t)bh * a.NC + c) * D * kChunk;
@@ -549,85 +558,70 @@ __global__ __launch_bounds__(BQ * 2) void routed_attn_kernel(AttnArgs a) {
             nrows = min(kBlockK, a.N - code * kBlockK);
             vstride = a.Npad;
         }
+        char* stage = smem + buf * L::STAGE;
 #pragma unroll
-        for (int u = 0; u < KCH; ++u) {
-            const int ch = tid + u * NT, row = ch / (D / 8), c8 = ch % (D / 8);
-            kr[u] = row < nrows ? *reinterpret_cast<const u32x4*>(kp + (size_t)row * D + c8 * 8) : u32x4{};
+        for (int u = 0; u < KPW; ++u) {
+            const int w0 = (wave * KPW + u) * 64;          // first chunk position of this load
+            const int r = (w0 + lane) / L::KCPR;
+            const int c = (lane % L::KCPR) ^ (r & (L::KCPR - 1));
+            const int off = min(r, nrows - 1) * D + c * 8;  // 32-bit element offset
+            __builtin_amdgcn_global_load_lds(kp + off, (lds_ptr_t)(stage + w0 * 16), 16, 0, 0);
         }
 #pragma unroll
-        for (int u = 0; u < VCH; ++u) {
-            const int ch = tid + u * NT, drow = ch / 8, p8 = ch % 8;
-            vr[u] = *reinterpret_cast<const u32x4*>(vp + (size_t)drow * vstride + p8 * 8);
-        }
-    };
-    auto stash = [&](int buf) {
-#pragma unroll
-        for (int u = 0; u < KCH; ++u) {
-            const int ch = tid + u * NT, row = ch / (D / 8), c8 = ch % (D / 8);
-            *reinterpret_cast<u32x4*>(kbuf(buf) + row * KS + c8 * 8) = kr[u];
-        }
-#pragma unroll
-        for (int u = 0; u < VCH; ++u) {
-            const int ch = tid + u * NT, drow = ch / 8, p8 = ch % 8;
-            *reinterpret_cast<u32x4*>(vbuf(buf) + drow * VS + p8 * 8) = vr[u];
+        for (int u = 0; u < VPW; ++u) {
+            const int w0 = (wave * VPW + u) * 64;
+            const int r = (w0 + lane) / L::VCPR;
+            const int c = (lane % L::VCPR) ^ (r & (L::VCPR - 1));
+            const int off = r * vstride + c * 8;
+            __builtin_amdgcn_global_load_lds(vp + off, (lds_ptr_t)(stage + L::KBYTES + w0 * 16), 16, 0, 0);
         }
     };
-
-    if (ntiles > 0) {
-        fetch(tile_code(0));
-        stash(0);
-    }
-    __syncthreads();
 
     const float cl = a.c_log2;
-    for (int n = 0; n < ntiles; ++n) {
+    // One tile: S^T = K Q^T, masks, online softmax, O^T += V^T P^T.  APX selects the
+    // correction-tile variant (f16 pooled keys x f16 queries, multiplicity bias, exclusion of
+    // selected and non-routable slots); exact tiles use bf16 keys x bf16 queries.
+    auto tile = [&](auto apx_tag, int n, const auto& qop) {
+        constexpr bool APX = decltype(apx_tag)::value;
         const int code = tile_code(n);
         const int buf = n & 1;
-        const bool more = n + 1 < ntiles;
-        if (more) fetch(tile_code(n + 1));
+        if (n + 1 < ntiles) issue(tile_code(n + 1), buf ^ 1);
+        const char* Kb = smem + buf * L::STAGE;
+        const char* Vb = Kb + L::KBYTES;
 
-        const uint16_t* Kb = kbuf(buf);
-        const _Float16* Vb = vbuf(buf);
-
-        // ---- S^T = K Q^T  (two 32-key M-tiles).  Exact tiles: bf16 keys and queries.
-        // Correction tiles: f16 pooled keys against an f16 copy of the queries (exact for
-        // bf16 values in the f16 range), so the pooled keys keep 11 significant bits.
         f32x16 s0 = f32x16{}, s1 = f32x16{};
-        if (code & kApxFlag) {
 #pragma unroll
-            for (int ks = 0; ks < NKS; ++ks) {
-                f16x8 qh;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) qh[e] = (_Float16)(float)qf[ks][e];
-                const f16x8 a0 = *reinterpret_cast<const f16x8*>(Kb + r32 * KS + 16 * ks + 8 * hh);
-                const f16x8 a1 = *reinterpret_cast<const f16x8*>(Kb + (32 + r32) * KS + 16 * ks + 8 * hh);
-                s0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a0, qh, s0, 0, 0, 0);
-                s1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a1, qh, s1, 0, 0, 0);
-            }
-        } else {
-#pragma unroll
-            for (int ks = 0; ks < NKS; ++ks) {
-                const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(Kb + r32 * KS + 16 * ks + 8 * hh);
-                const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(Kb + (32 + r32) * KS + 16 * ks + 8 * hh);
-                s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qf[ks], s0, 0, 0, 0);
-                s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qf[ks], s1, 0, 0, 0);
+        for (int ks = 0; ks < NKS; ++ks) {
+            if constexpr (APX) {
+                const f16x8 a0 = *reinterpret_cast<const f16x8*>(Kb + 16 * L::kpos(r32, 2 * ks + hh));
+                const f16x8 a1 = *reinterpret_cast<const f16x8*>(Kb + 16 * L::kpos(32 + r32, 2 * ks + hh));
+                s0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a0, qop[ks], s0, 0, 0, 0);
+                s1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a1, qop[ks], s1, 0, 0, 0);
+            } else {
+                const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(Kb + 16 * L::kpos(r32, 2 * ks + hh));
+                const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(Kb + 16 * L::kpos(32 + r32, 2 * ks + hh));
+                s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qop[ks], s0, 0, 0, 0);
+                s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qop[ks], s1, 0, 0, 0);
             }
         }
 
-        // ---- masks: ragged last key block, or correction-tile multiplicity / exclusion
-        if (code & kApxFlag) {
+        if constexpr (APX) {
+            // slot j of the chunk contributes with log2(n_j) (multiplicity of Eq.
+            // solattn_denominator) unless it is selected (exact tile) or past the routable keys
             const int c = code & ~kApxFlag;
-            auto apx_bias = [&](int j) -> float {  // log2(n_j) in raw-logit units, or -inf
-                bool ok = j < a.NKr;
-                if (ok) ok = !((selw[j >> 5] >> (j & 31)) & 1u);
-                const int nj = min(kBlockK, a.N - j * kBlockK);
-                return ok ? __log2f((float)nj) / cl : kNegInf;
+            const uint32_t wlo = selw[2 * c];
+            const uint32_t whi = 2 * c + 1 < a.MW ? selw[2 * c + 1] : 0u;
+            const int nvalid = min(kChunk, a.NKr - c * kChunk);
+            const int last_slot = a.NK - 1 - c * kChunk;   // slot of the (possibly short) last block
+            auto apx_bias = [&](int slot, uint32_t word) -> float {
+                const bool ok = slot < nvalid && !((word >> (slot & 31)) & 1u);
+                return ok ? (slot == last_slot ? a.bias_last : a.bias_full) : kNegInf;
             };
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int slot0 = 8 * (r >> 2) + 4 * hh + (r & 3);
-                s0[r] += apx_bias(c * kChunk + slot0);
-                s1[r] += apx_bias(c * kChunk + 32 + slot0);
+                s0[r] += apx_bias(slot0, wlo);
+                s1[r] += apx_bias(32 + slot0, whi);
             }
         } else {
             const int nvalid = a.N - code * kBlockK;
@@ -641,7 +635,7 @@ __global__ __launch_bounds__(BQ * 2) void routed_attn_kernel(AttnArgs a) {
             }
         }
 
-        // ---- online softmax (log2 domain, lazy rescale)
+        // online softmax (log2 domain, lazy rescale)
         float mx = kNegInf;
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
@@ -678,26 +672,49 @@ __global__ __launch_bounds__(BQ * 2) void routed_attn_kernel(AttnArgs a) {
             }
         }
 
-        // ---- O^T += V^T P^T
+        // O^T += V^T P^T
 #pragma unroll
         for (int mt = 0; mt < NDT; ++mt) {
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk) {
-                const f16x8 av = *reinterpret_cast<const f16x8*>(Vb + (32 * mt + r32) * VS + 16 * kk + 8 * hh);
+                const f16x8 av = *reinterpret_cast<const f16x8*>(Vb + 16 * L::vpos(32 * mt + r32, 2 * kk + hh));
                 o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, pb[kk], o[mt], 0, 0, 0);
             }
         }
 
-        if (more) stash(buf ^ 1);
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
+    };
+
+    if (ntiles > 0) issue(tile_code(0), 0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+
+    // Correction tiles (sparse mode): queries as f16 (exact for bf16 values in the f16 range).
+    if (MODE == kSparse && napx > 0) {
+        f16x8 qh[NKS];
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+            const bf16x8 qv = qrow < a.N ? *reinterpret_cast<const bf16x8*>(qrow_p + 16 * ks) : bf16x8{};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) qh[ks][e] = (_Float16)(float)qv[e];
+        }
+        for (int n = 0; n < napx; ++n) tile(std::integral_constant<bool, true>{}, n, qh);
+    }
+    // Exact tiles: bf16 queries.
+    {
+        bf16x8 qf[NKS];
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks)
+            qf[ks] = qrow < a.N ? *reinterpret_cast<const bf16x8*>(qrow_p + 16 * ks) : bf16x8{};
+        for (int n = napx; n < ntiles; ++n) tile(std::integral_constant<bool, false>{}, n, qf);
     }
 
     // ---- epilogue: O = O^T / l, bf16
     const float lt = l_run + __shfl_xor(l_run, 32);
     const float inv = lt > 0.f ? 1.0f / lt : 0.f;
-    const int row = qi * BQ + wave * 32 + r32;
-    if (row < a.N) {
-        uint16_t* op = a.out + ((size_t)bh * a.N + row) * D;
+    if (qrow < a.N) {
+        uint16_t* op = a.out + ((size_t)bh * a.N + qrow) * D;
 #pragma unroll
         for (int mt = 0; mt < NDT; ++mt) {
 #pragma unroll
@@ -747,14 +764,14 @@ __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
     int* list = reinterpret_cast<int*>(rest + 64 + 4 * D + 4 * ((a.MW + 3) & ~3));
 
     const int bh = blockIdx.y, qi = blockIdx.x, tid = threadIdx.x;
-    int ntiles, nsel;
+    int ntiles, nsel, napx = 0;
     if (MODE == kDense) {
         ntiles = a.NK;
         nsel = a.NKr;
     } else {
         ntiles = route_and_list<D, NT, MODE>(a.qbar + ((size_t)bh * a.NQ + qi) * D, a.kbar + (size_t)bh * a.NK * D,
                                              a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, qb_s,
-                                             selw, list, scan_scratch, &nsel);
+                                             selw, list, scan_scratch, &napx, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
@@ -910,7 +927,7 @@ Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype
 size_t attn_lds_bytes(const Shape& s) {
     const size_t rest = 64 + 4 * (size_t)s.d + 4 * (size_t)((s.MW + 3) & ~3) + 4 * (size_t)(s.NK + s.NC);
     if (s.dtype == kBF16) {
-        const size_t stage = (size_t)kBlockK * (s.d + 8) * 2 + (size_t)s.d * (kBlockK + 8) * 2;
+        const size_t stage = (size_t)kBlockK * s.d * 2 * 2;
         return 2 * stage + rest;
     }
     return (size_t)2 * kBlockK * s.d * 4 + (size_t)s.d * s.bq * 4 + rest;
@@ -1022,6 +1039,8 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         a.per_x = (s.NQ + 7) / 8;
         a.scale = scale;
         a.c_log2 = scale * kLog2e;
+        a.bias_full = log2f((float)kBlockK) / a.c_log2;
+        a.bias_last = log2f((float)(s.N - (s.NK - 1) * kBlockK)) / a.c_log2;
         if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
         if (d == 128) e = s.bq == 128 ? dispatch_bf16_mode<128, 128>(s, a, st) : dispatch_bf16_mode<128, 64>(s, a, st);
         else e = s.bq == 128 ? dispatch_bf16_mode<64, 128>(s, a, st) : dispatch_bf16_mode<64, 64>(s, a, st);
