@@ -34,12 +34,18 @@ def build(verbose: bool = False) -> str:
     os.makedirs(build_dir, exist_ok=True)
     for src in SOURCES:
         obj = os.path.join(build_dir, src + ".o")
-        lang = ["-x", "hip"] if src.endswith(".hip") else ["-x", "hip"]
-        cmd = [hipcc(), *lang, *common, "-c", os.path.join(CSRC, src), "-o", obj]
+        # Kernels never see NaN by contract (NaN inputs are invalid); this lets max() skip
+        # NaN canonicalisation of MFMA results.  Infinities keep their IEEE meaning.
+        extra = ["-fno-honor-nans"] if src.endswith(".hip") else []
+        cmd = [hipcc(), "-x", "hip", *common, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
         _run(cmd, verbose)
         objs.append(obj)
     tmp = LIB + ".tmp"
     _run([hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
+    # An unresolved kernel handle (e.g. a kernel the host pass dropped) only shows up at
+    # load time: load the fresh library once so such a build fails here.
+    import ctypes
+    ctypes.CDLL(tmp)
     os.replace(tmp, LIB)
     return LIB
 

@@ -382,31 +382,67 @@ __device__ int block_scan_incl(int v, int* scratch, int* total) {
 template <int D, int NT, int MODE>
 __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __restrict__ kbar_h, float tau_i,
                               float scale, int NKr, int NK, int MW, int NC, float* qb_s, uint32_t* selw,
-                              int* list, int* scan_scratch, int* napx, int* nsel) {
+                              char* stages, int* list, int* scan_scratch, int* napx, int* nsel) {
+    constexpr int NW = NT / 64;
+    constexpr int CPR = D / 4;              // 16-byte chunks per f32 pooled-key row
+    constexpr int WL = CPR / NW;            // wave loads per wave for one chunk of 64 rows
+    constexpr int TPK = NT / kChunk;        // threads per pooled key (1, 2 or 4)
+    constexpr int KPWV = 64 / TPK;          // pooled keys per wave (64, 32 or 16)
+    static_assert(NT % kChunk == 0 && TPK <= 4, "routing expects 64..256 threads");
+    constexpr int STAGE = kChunk * D * 4;   // one chunk of f32 pooled keys == one tile stage
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int c = tid; c < D; c += NT) qb_s[c] = qbar_i[c];
-    __syncthreads();
-    for (int base = 0; base < NKr; base += NT) {
-        const int j = base + tid;
-        bool sel = false;
-        if (j < NKr) {
-            const f32x4* kp = reinterpret_cast<const f32x4*>(kbar_h + (size_t)j * D);
-            float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
-#pragma unroll 8
-            for (int c4 = 0; c4 < D / 4; ++c4) {
-                const f32x4 kv = kp[c4];
-                a0 = fmaf(qb_s[4 * c4 + 0], kv[0], a0);
-                a1 = fmaf(qb_s[4 * c4 + 1], kv[1], a1);
-                a2 = fmaf(qb_s[4 * c4 + 2], kv[2], a2);
-                a3 = fmaf(qb_s[4 * c4 + 3], kv[3], a3);
-            }
-            sel = scale * ((a0 + a1) + (a2 + a3)) > tau_i;
+    for (int w = tid; w < MW; w += NT) selw[w] = 0u;
+    // Chunk c of pooled keys -> stage (c & 1); row r's 16-byte chunk cc sits at position
+    // r*CPR + (cc ^ (4r mod CPR)) so that the 4-lane groups below read distinct banks.
+    auto issue = [&](int c, int buf) {
+        char* st = stages + buf * STAGE;
+#pragma unroll
+        for (int u = 0; u < WL; ++u) {
+            const int w0 = (wave * WL + u) * 64;
+            const int r = (w0 + lane) / CPR;
+            const int cc = (lane % CPR) ^ ((4 * r) & (CPR - 1));
+            const int row = min(c * kChunk + r, NKr - 1);
+            __builtin_amdgcn_global_load_lds(kbar_h + (size_t)row * D + cc * 4,
+                                             (__attribute__((address_space(3))) void*)(st + w0 * 16), 16, 0, 0);
         }
+    };
+    issue(0, 0);
+    const int jl = tid / TPK, seg = tid % TPK;
+    for (int c = 0; c < NC; ++c) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        if (c + 1 < NC) issue(c + 1, (c + 1) & 1);
+        const char* st = stages + (c & 1) * STAGE;
+        float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+        for (int i = 0; i < CPR / TPK; ++i) {
+            const int cc = seg + TPK * i;
+            const f32x4 kv = *reinterpret_cast<const f32x4*>(st + 16 * (jl * CPR + (cc ^ ((4 * jl) & (CPR - 1)))));
+            a0 = fmaf(qb_s[4 * cc + 0], kv[0], a0);
+            a1 = fmaf(qb_s[4 * cc + 1], kv[1], a1);
+            a2 = fmaf(qb_s[4 * cc + 2], kv[2], a2);
+            a3 = fmaf(qb_s[4 * cc + 3], kv[3], a3);
+        }
+        float dot = (a0 + a1) + (a2 + a3);
+#pragma unroll
+        for (int off = 1; off < TPK; off <<= 1) dot += __shfl_xor(dot, off);
+        const int j = c * kChunk + jl;
+        const bool sel = j < NKr && scale * dot > tau_i;
         const uint64_t bal = __ballot(sel);
+        uint64_t bits = 0;
+#pragma unroll
+        for (int t = 0; t < KPWV; ++t) bits |= ((bal >> (TPK * t)) & 1ull) << t;
         if (lane == 0) {
-            const int w0 = (base + wave * 64) >> 5;
-            if (w0 < MW) selw[w0] = (uint32_t)bal;
-            if (w0 + 1 < MW) selw[w0 + 1] = (uint32_t)(bal >> 32);
+            const int bit0 = c * kChunk + wave * KPWV;
+            if constexpr (KPWV == 64) {
+                selw[bit0 >> 5] = (uint32_t)bits;
+                selw[(bit0 >> 5) + 1] = (uint32_t)(bits >> 32);
+            } else if constexpr (KPWV == 32) {
+                selw[bit0 >> 5] = (uint32_t)bits;
+            } else {
+                reinterpret_cast<uint16_t*>(selw)[bit0 >> 4] = (uint16_t)bits;
+            }
         }
     }
     __syncthreads();
@@ -508,7 +544,8 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     const int qi = xcd * a.per_x + (y % a.per_x);
     if (bh >= a.BH || qi >= a.NQ) return;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, kept in an SGPR
     const int r32 = lane & 31, hh = lane >> 5;
 
     char* rest = smem + 2 * L::STAGE;
@@ -524,7 +561,7 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     } else {
         ntiles = route_and_list<D, NT, MODE>(a.qbar + ((size_t)bh * a.NQ + qi) * D, a.kbar + (size_t)bh * a.NK * D,
                                              a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, qb_s,
-                                             selw, list, scan_scratch, &napx, &nsel);
+                                             selw, smem, list, scan_scratch, &napx, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
@@ -539,107 +576,155 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     float m_run = kNegInf, l_run = 0.f;
 
     auto tile_code = [&](int n) -> int { return MODE == kDense ? n : list[n]; };
-    // Issue the global->LDS copies of tile `code` into stage `buf`.  Each lane moves one
-    // 16-byte chunk per instruction; rows past the end of the sequence are clamped to the
-    // last valid row (their scores are masked to -inf, their values are zero in V^T).
-    auto issue = [&](int code, int buf) {
-        const uint16_t* kp;
-        const _Float16* vp;
-        int nrows, vstride;
-        if (MODE != kDense && (code & kApxFlag)) {
-            const int c = code & ~kApxFlag;
-            kp = reinterpret_cast<const uint16_t*>(a.kbarh) + ((size_t)bh * a.NC * kChunk + (size_t)c * kChunk) * D;
-            vp = a.vbart + ((size_t)bh * a.NC + c) * D * kChunk;
-            nrows = kChunk;
-            vstride = kChunk;
-        } else {
-            kp = a.k + ((size_t)bh * a.N + (size_t)code * kBlockK) * D;
-            vp = a.vt + (size_t)bh * D * a.Npad + (size_t)code * kBlockK;
-            nrows = min(kBlockK, a.N - code * kBlockK);
-            vstride = a.Npad;
-        }
-        char* stage = smem + buf * L::STAGE;
+    // Global->LDS copies.  Each lane moves one 16-byte chunk per instruction; the per-lane
+    // byte offsets inside a tile are fixed, so they are computed once here and each tile only
+    // adds wave-uniform base pointers.  Rows past the end of the sequence (ragged last block)
+    // are clamped to the last valid row: their scores are masked to -inf and their values
+    // are zero in V^T.
+    uint32_t koff[KPW], voff[VPW];
 #pragma unroll
-        for (int u = 0; u < KPW; ++u) {
-            const int w0 = (wave * KPW + u) * 64;          // first chunk position of this load
-            const int r = (w0 + lane) / L::KCPR;
-            const int c = (lane % L::KCPR) ^ (r & (L::KCPR - 1));
-            const int off = min(r, nrows - 1) * D + c * 8;  // 32-bit element offset
-            __builtin_amdgcn_global_load_lds(kp + off, (lds_ptr_t)(stage + w0 * 16), 16, 0, 0);
-        }
+    for (int u = 0; u < KPW; ++u) {
+        const int r = ((wave * KPW + u) * 64 + lane) / L::KCPR;
+        const int c = (lane % L::KCPR) ^ (r & (L::KCPR - 1));
+        koff[u] = (uint32_t)(r * D + c * 8) * 2u;
+    }
+#pragma unroll
+    for (int u = 0; u < VPW; ++u) {
+        const int r = ((wave * VPW + u) * 64 + lane) / L::VCPR;
+        const int c = (lane % L::VCPR) ^ (r & (L::VCPR - 1));
+        voff[u] = (uint32_t)(r * a.Npad + c * 8) * 2u;
+    }
+    // Copies of a correction tile (pooled keys of chunk c and their value means) ...
+    auto issue_apx = [&](int c, int buf) {
+        char* stage = smem + buf * L::STAGE;
+        const char* kp = reinterpret_cast<const char*>(a.kbarh + ((size_t)bh * a.NC * kChunk + (size_t)c * kChunk) * D);
+        const char* vp = reinterpret_cast<const char*>(a.vbart + ((size_t)bh * a.NC + c) * D * kChunk);
+#pragma unroll
+        for (int u = 0; u < KPW; ++u)
+            __builtin_amdgcn_global_load_lds((const void*)(kp + koff[u]), (lds_ptr_t)(stage + (wave * KPW + u) * 1024),
+                                             16, 0, 0);
 #pragma unroll
         for (int u = 0; u < VPW; ++u) {
-            const int w0 = (wave * VPW + u) * 64;
-            const int r = (w0 + lane) / L::VCPR;
+            const int r = ((wave * VPW + u) * 64 + lane) / L::VCPR;
             const int c = (lane % L::VCPR) ^ (r & (L::VCPR - 1));
-            const int off = r * vstride + c * 8;
-            __builtin_amdgcn_global_load_lds(vp + off, (lds_ptr_t)(stage + L::KBYTES + w0 * 16), 16, 0, 0);
+            const uint32_t off = (uint32_t)(r * kChunk + c * 8) * 2u;
+            __builtin_amdgcn_global_load_lds((const void*)(vp + off),
+                                             (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024), 16, 0, 0);
         }
+    };
+    // ... and of an exact tile: key block j into stage `buf`'s K region ...
+    auto issue_exact_k = [&](int j, int buf) {
+        char* stage = smem + buf * L::STAGE;
+        const char* kp = reinterpret_cast<const char*>(a.k + ((size_t)bh * a.N + (size_t)j * kBlockK) * D);
+        const int nrows = a.N - j * kBlockK;
+        if (nrows >= kBlockK) {
+#pragma unroll
+            for (int u = 0; u < KPW; ++u)
+                __builtin_amdgcn_global_load_lds((const void*)(kp + koff[u]),
+                                                 (lds_ptr_t)(stage + (wave * KPW + u) * 1024), 16, 0, 0);
+        } else {
+#pragma unroll
+            for (int u = 0; u < KPW; ++u) {
+                const int r = ((wave * KPW + u) * 64 + lane) / L::KCPR;
+                const int c = (lane % L::KCPR) ^ (r & (L::KCPR - 1));
+                const uint32_t off = (uint32_t)(min(r, nrows - 1) * D + c * 8) * 2u;
+                __builtin_amdgcn_global_load_lds((const void*)(kp + off), (lds_ptr_t)(stage + (wave * KPW + u) * 1024),
+                                                 16, 0, 0);
+            }
+        }
+    };
+    // ... and its transposed values into stage `buf`'s V region.
+    auto issue_exact_v = [&](int j, int buf) {
+        char* stage = smem + buf * L::STAGE;
+        const char* vp = reinterpret_cast<const char*>(a.vt + (size_t)bh * D * a.Npad + (size_t)j * kBlockK);
+#pragma unroll
+        for (int u = 0; u < VPW; ++u)
+            __builtin_amdgcn_global_load_lds((const void*)(vp + voff[u]),
+                                             (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024), 16, 0, 0);
     };
 
     const float cl = a.c_log2;
-    // One tile: S^T = K Q^T, masks, online softmax, O^T += V^T P^T.  APX selects the
-    // correction-tile variant (f16 pooled keys x f16 queries, multiplicity bias, exclusion of
-    // selected and non-routable slots); exact tiles use bf16 keys x bf16 queries.
-    auto tile = [&](auto apx_tag, int n, const auto& qop) {
-        constexpr bool APX = decltype(apx_tag)::value;
-        const int code = tile_code(n);
-        const int buf = n & 1;
-        if (n + 1 < ntiles) issue(tile_code(n + 1), buf ^ 1);
-        const char* Kb = smem + buf * L::STAGE;
-        const char* Vb = Kb + L::KBYTES;
 
-        f32x16 s0 = f32x16{}, s1 = f32x16{};
+    // ---- building blocks of a tile -------------------------------------------------------
+    // LDS operand addresses: per lane, the chunk read at k-step ks of a K tile and at k-step
+    // kk of a V^T tile (rows r32 and 32+r32 of K share the swizzle; the second M-tile is a
+    // constant 8 KB further, V^T M-tiles 4 KB apart).  With the stage fixed at compile time
+    // every operand read is base register + immediate offset.
+    uint32_t kadr[NKS], vadr[4];
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) kadr[ks] = 16u * (uint32_t)L::kpos(r32, 2 * ks + hh);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) vadr[kk] = (uint32_t)L::KBYTES + 16u * (uint32_t)L::vpos(r32, 2 * kk + hh);
+    constexpr int KT1 = 32 * L::KCPR * 16;   // byte offset of K rows 32..63
+    constexpr int VMT = 32 * L::VCPR * 16;   // byte offset between V^T M-tiles
+
+    // S^T = K Q^T over two 32-key M-tiles, operands double-buffered in registers.  Exact
+    // tiles: bf16 keys x bf16 queries.  Correction tiles: f16 pooled keys x f16 queries, so the
+    // pooled keys keep 11 significant bits.
+    auto qk = [&](auto apx_tag, auto stage_tag, const auto& qop, f32x16& s0, f32x16& s1) {
+        constexpr bool APX = decltype(apx_tag)::value;
+        constexpr int SOFF = decltype(stage_tag)::value * L::STAGE;
+        using AT = std::conditional_t<APX, f16x8, bf16x8>;
+        AT a0[2], a1[2];
+        a0[0] = *reinterpret_cast<const AT*>(smem + kadr[0] + SOFF);
+        a1[0] = *reinterpret_cast<const AT*>(smem + kadr[0] + SOFF + KT1);
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
+            if (ks + 1 < NKS) {
+                a0[(ks + 1) & 1] = *reinterpret_cast<const AT*>(smem + kadr[ks + 1] + SOFF);
+                a1[(ks + 1) & 1] = *reinterpret_cast<const AT*>(smem + kadr[ks + 1] + SOFF + KT1);
+            }
             if constexpr (APX) {
-                const f16x8 a0 = *reinterpret_cast<const f16x8*>(Kb + 16 * L::kpos(r32, 2 * ks + hh));
-                const f16x8 a1 = *reinterpret_cast<const f16x8*>(Kb + 16 * L::kpos(32 + r32, 2 * ks + hh));
-                s0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a0, qop[ks], s0, 0, 0, 0);
-                s1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a1, qop[ks], s1, 0, 0, 0);
+                s0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a0[ks & 1], qop[ks], s0, 0, 0, 0);
+                s1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a1[ks & 1], qop[ks], s1, 0, 0, 0);
             } else {
-                const bf16x8 a0 = *reinterpret_cast<const bf16x8*>(Kb + 16 * L::kpos(r32, 2 * ks + hh));
-                const bf16x8 a1 = *reinterpret_cast<const bf16x8*>(Kb + 16 * L::kpos(32 + r32, 2 * ks + hh));
-                s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, qop[ks], s0, 0, 0, 0);
-                s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, qop[ks], s1, 0, 0, 0);
+                s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[ks & 1], qop[ks], s0, 0, 0, 0);
+                s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks & 1], qop[ks], s1, 0, 0, 0);
             }
         }
-
-        if constexpr (APX) {
-            // slot j of the chunk contributes with log2(n_j) (multiplicity of Eq.
-            // solattn_denominator) unless it is selected (exact tile) or past the routable keys
-            const int c = code & ~kApxFlag;
-            const uint32_t wlo = selw[2 * c];
-            const uint32_t whi = 2 * c + 1 < a.MW ? selw[2 * c + 1] : 0u;
-            const int nvalid = min(kChunk, a.NKr - c * kChunk);
-            const int last_slot = a.NK - 1 - c * kChunk;   // slot of the (possibly short) last block
-            auto apx_bias = [&](int slot, uint32_t word) -> float {
-                const bool ok = slot < nvalid && !((word >> (slot & 31)) & 1u);
-                return ok ? (slot == last_slot ? a.bias_last : a.bias_full) : kNegInf;
-            };
+    };
+    // Keys past the end of the sequence (only in the last key block) -> -inf.
+    auto mask_tail = [&](int j, f32x16& s0, f32x16& s1) {
+        const int nvalid = a.N - j * kBlockK;
+        if (nvalid < kBlockK) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                const int slot0 = 8 * (r >> 2) + 4 * hh + (r & 3);
-                s0[r] += apx_bias(slot0, wlo);
-                s1[r] += apx_bias(32 + slot0, whi);
-            }
-        } else {
-            const int nvalid = a.N - code * kBlockK;
-            if (nvalid < kBlockK) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int key0 = 8 * (r >> 2) + 4 * hh + (r & 3);
-                    if (key0 >= nvalid) s0[r] = kNegInf;
-                    if (32 + key0 >= nvalid) s1[r] = kNegInf;
-                }
+                const int key0 = 8 * (r >> 2) + 4 * hh + (r & 3);
+                if (key0 >= nvalid) s0[r] = kNegInf;
+                if (32 + key0 >= nvalid) s1[r] = kNegInf;
             }
         }
-
-        // online softmax (log2 domain, lazy rescale)
+    };
+    // Correction tile of chunk c: slot j contributes with log2(n_j) (the multiplicity of Eq.
+    // solattn_denominator) unless it is selected (exact tile) or past the routable keys.
+    auto bias_apx = [&](int c, f32x16& s0, f32x16& s1) {
+        const uint32_t wlo = selw[2 * c];
+        const uint32_t whi = 2 * c + 1 < a.MW ? selw[2 * c + 1] : 0u;
+        const int nvalid = min(kChunk, a.NKr - c * kChunk);
+        const int last_slot = a.NK - 1 - c * kChunk;   // slot of the (possibly short) last block
+        auto apx_bias = [&](int slot, uint32_t word) -> float {
+            const bool ok = slot < nvalid && !((word >> (slot & 31)) & 1u);
+            return ok ? (slot == last_slot ? a.bias_last : a.bias_full) : kNegInf;
+        };
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int slot0 = 8 * (r >> 2) + 4 * hh + (r & 3);
+            s0[r] += apx_bias(slot0, wlo);
+            s1[r] += apx_bias(32 + slot0, whi);
+        }
+    };
+    // Online softmax in the log2 domain with lazy rescaling, split so that the (rarely
+    // taken) rescale branch sits apart from the MFMA/VALU stream:
+    //   tile_max  - row max of a score tile (both lane halves of a query agree)
+    //   rescale   - raise the running max if a tile exceeds it by more than kRescaleSlack
+    //   exps      - P^T = exp2(S*c - m) packed as f16 B operands; row sums from the rounded P
+    auto tile_max = [&](const f32x16& s0, const f32x16& s1) -> float {
         float mx = kNegInf;
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        return fmaxf(mx, __shfl_xor(mx, 32));
+    };
+    auto rescale = [&](float mx) {
         const float mt_ = mx * cl;
         const bool need = mt_ > m_run + kRescaleSlack;
         if (__ballot(need)) {
@@ -650,8 +735,9 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
             l_run *= alpha;
             m_run = mnew;
         }
+    };
+    auto exps = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[4]) {
         const float msub = m_run == kNegInf ? 0.f : m_run;
-        f16x8 pb[4];
         const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
 #pragma unroll
         for (int tt = 0; tt < 2; ++tt) {
@@ -671,26 +757,32 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
                 }
             }
         }
-
-        // O^T += V^T P^T
-#pragma unroll
-        for (int mt = 0; mt < NDT; ++mt) {
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                const f16x8 av = *reinterpret_cast<const f16x8*>(Vb + 16 * L::vpos(32 * mt + r32, 2 * kk + hh));
-                o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, pb[kk], o[mt], 0, 0, 0);
-            }
-        }
-
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
     };
+    auto softmax = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[4]) {
+        rescale(tile_max(s0, s1));
+        exps(s0, s1, pb);
+    };
+    // O^T += V^T P^T, operands double-buffered in registers.
+    auto pv = [&](auto stage_tag, const f16x8 (&pb)[4]) {
+        constexpr int SOFF = decltype(stage_tag)::value * L::STAGE;
+        f16x8 av[2];
+        av[0] = *reinterpret_cast<const f16x8*>(smem + vadr[0] + SOFF);
+#pragma unroll
+        for (int i = 0; i < NDT * 4; ++i) {
+            const int mt = i >> 2, kk = i & 3;
+            if (i + 1 < NDT * 4) {
+                const int mt1 = (i + 1) >> 2, kk1 = (i + 1) & 3;
+                av[(i + 1) & 1] = *reinterpret_cast<const f16x8*>(smem + vadr[kk1] + SOFF + mt1 * VMT);
+            }
+            o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i & 1], pb[kk], o[mt], 0, 0, 0);
+        }
+    };
+    using S0 = std::integral_constant<int, 0>;
+    using S1 = std::integral_constant<int, 1>;
+    using APX_T = std::integral_constant<bool, true>;
+    using EXACT_T = std::integral_constant<bool, false>;
 
-    if (ntiles > 0) issue(tile_code(0), 0);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-
-    // Correction tiles (sparse mode): queries as f16 (exact for bf16 values in the f16 range).
+    // ---- correction tiles (sparse mode): one stage per tile, prefetch one tile ahead -------
     if (MODE == kSparse && napx > 0) {
         f16x8 qh[NKS];
 #pragma unroll
@@ -699,15 +791,80 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
 #pragma unroll
             for (int e = 0; e < 8; ++e) qh[ks][e] = (_Float16)(float)qv[e];
         }
-        for (int n = 0; n < napx; ++n) tile(std::integral_constant<bool, true>{}, n, qh);
+        issue_apx(list[0] & ~kApxFlag, 0);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        auto apx_tile = [&](auto stage_tag, int n) {
+            constexpr int ST = decltype(stage_tag)::value;
+            const int c = list[n] & ~kApxFlag;
+            if (n + 1 < napx) issue_apx(list[n + 1] & ~kApxFlag, ST ^ 1);
+            f32x16 s0 = f32x16{}, s1 = f32x16{};
+            qk(APX_T{}, stage_tag, qh, s0, s1);
+            bias_apx(c, s0, s1);
+            f16x8 pb[4];
+            softmax(s0, s1, pb);
+            pv(stage_tag, pb);
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+        };
+        for (int n = 0; n < napx; n += 2) {
+            apx_tile(S0{}, n);
+            if (n + 1 < napx) apx_tile(S1{}, n + 1);
+        }
     }
-    // Exact tiles: bf16 queries.
-    {
+
+    // ---- exact tiles: software-pipelined, keys one tile ahead of values --------------------
+    // Iteration t computes the scores of tile t+1 (MFMA) while the softmax of tile t (VALU)
+    // runs, then O += V_t P_t.  Stage b's K region holds tile t+1 while its V region still
+    // holds tile t, so both stages are busy without a third buffer.  The loop is unrolled by
+    // two so that the stage of every LDS access is a compile-time offset.
+    const int T = ntiles - napx;
+    auto ecode = [&](int t) -> int { return tile_code(napx + t); };
+    if (T > 0) {
         bf16x8 qf[NKS];
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks)
             qf[ks] = qrow < a.N ? *reinterpret_cast<const bf16x8*>(qrow_p + 16 * ks) : bf16x8{};
-        for (int n = napx; n < ntiles; ++n) tile(std::integral_constant<bool, false>{}, n, qf);
+        issue_exact_k(ecode(0), 0);
+        issue_exact_v(ecode(0), 0);
+        if (T > 1) issue_exact_k(ecode(1), 1);
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        f32x16 s0 = f32x16{}, s1 = f32x16{};
+        qk(EXACT_T{}, S0{}, qf, s0, s1);
+        float mx = tile_max(s0, s1);
+        // iteration t with t & 1 == P: K of tile t+1 in stage P^1, V of tile t in stage P
+        auto step = [&](auto par_tag, int t) {
+            constexpr int P = decltype(par_tag)::value;
+            rescale(mx);
+            if (t + 2 < T) issue_exact_k(ecode(t + 2), P);
+            issue_exact_v(ecode(t + 1), P ^ 1);
+            f32x16 n0 = f32x16{}, n1 = f32x16{};
+            qk(EXACT_T{}, std::integral_constant<int, P ^ 1>{}, qf, n0, n1);
+            f16x8 pb[4];
+            exps(s0, s1, pb);         // tile t is never the ragged last block here
+            pv(par_tag, pb);
+            mx = tile_max(n0, n1);
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+            s0 = n0;
+            s1 = n1;
+        };
+        int t = 0;
+        for (; t + 2 < T; t += 2) {
+            step(S0{}, t);
+            step(S1{}, t + 1);
+        }
+        if (t + 1 < T) {
+            step(S0{}, t);
+            ++t;
+        }
+        // last tile (t == T-1): the only one that can be the ragged last key block
+        mask_tail(ecode(T - 1), s0, s1);
+        f16x8 pb[4];
+        softmax(s0, s1, pb);
+        if ((T - 1) & 1) pv(S1{}, pb);
+        else pv(S0{}, pb);
     }
 
     // ---- epilogue: O = O^T / l, bf16
@@ -771,7 +928,7 @@ __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
     } else {
         ntiles = route_and_list<D, NT, MODE>(a.qbar + ((size_t)bh * a.NQ + qi) * D, a.kbar + (size_t)bh * a.NK * D,
                                              a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, qb_s,
-                                             selw, list, scan_scratch, &napx, &nsel);
+                                             selw, smem, list, scan_scratch, &napx, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
