@@ -132,11 +132,13 @@ int sol_attn_thresholds(const float* qbar, const float* kbar, float* tau, float*
     const int BH = B * H;
     // Moment buffers are temporary: allocate, run, wait, free (this entry point synchronises).
     void* mom = nullptr;
-    hipError_t e = hipMalloc(&mom, ((size_t)BH * d * d + (size_t)BH * d) * sizeof(float));
+    const size_t part = sol::moments_scratch_bytes(BH, d);
+    hipError_t e = hipMalloc(&mom, part + ((size_t)BH * d * d + (size_t)BH * d) * sizeof(float));
     if (e != hipSuccess) return hip_fail(e, "hipMalloc(moments)");
-    float* cov = static_cast<float*>(mom);
+    double* scratch = static_cast<double*>(mom);
+    float* cov = reinterpret_cast<float*>(static_cast<char*>(mom) + part);
     float* muk = cov + (size_t)BH * d * d;
-    e = sol::launch_moments(kbar, muk, cov, BH, NK, nk_routable, d, st);
+    e = sol::launch_moments(kbar, muk, cov, scratch, BH, NK, nk_routable, d, st);
     if (e == hipSuccess) e = sol::launch_tau(qbar, muk, cov, tau, mu, sigma, BH, NQ, d, beta, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
     (void)hipFree(mom);

@@ -36,6 +36,7 @@ struct Workspace {
     float* muk = nullptr;        // [BH][d]
     float* cov = nullptr;        // [BH][d][d]
     float* tau = nullptr;        // [BH][NQ]
+    double* mom = nullptr;       // partial moments, moments_scratch_bytes()
     uint32_t* blkcount = nullptr;// [BH][NQ]
 };
 
@@ -47,8 +48,9 @@ size_t attn_lds_bytes(const Shape& s);
 
 hipError_t launch_pool_mean(const void* x, float* mean, int dtype, int BH, int N, int d, int blk,
                             hipStream_t st);
-hipError_t launch_moments(const float* kbar, float* muk, float* cov, int BH, int NK, int NKr, int d,
-                          hipStream_t st);
+size_t moments_scratch_bytes(int BH, int d);
+hipError_t launch_moments(const float* kbar, float* muk, float* cov, double* scratch, int BH, int NK, int NKr,
+                          int d, hipStream_t st);
 hipError_t launch_tau(const float* qbar, const float* muk, const float* cov, float* tau, float* mu,
                       float* sigma, int BH, int NQ, int d, float beta, hipStream_t st);
 // ev_start/ev_stop (nullable) are recorded on `st` around the fused attention kernel.

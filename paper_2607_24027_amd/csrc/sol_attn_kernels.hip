@@ -228,55 +228,82 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict
 }
 
 // ---------------------------------------------------------------------------
-// Moments of the routable pooled keys (Eq. threshold_stats_exact, centred form).
-// grid (D/16, BH), 256 threads.  Every workgroup recomputes mu_K (f64 column sums) and then
-// owns 16 rows of C_K = mean_j (Kbar_j - mu_K)^T (Kbar_j - mu_K), accumulated in f64 from
-// 64-row slabs staged in LDS.
+// Moments of the routable pooled keys (Eq. threshold_stats_exact, centred form), in two
+// kernels.  moments_partial_kernel: grid (kMomSplit, BH), 256 threads; split s accumulates,
+// in f64, S1 = sum_j x_j and S2 = sum_j x_j^T x_j over its share of the key blocks, with
+// x_j = Kbar_j - Kbar_0 (a shift that keeps the second moment well conditioned).
+// moments_final_kernel: grid (BH), sums the splits and writes mu_K = Kbar_0 + S1/n and
+// C_K = S2/n - (S1/n)^T (S1/n) in f32.
 // ---------------------------------------------------------------------------
+constexpr int kMomSplit = 8;
+
 template <int D>
-__global__ __launch_bounds__(256) void moments_kernel(const float* __restrict__ kbar, float* __restrict__ muk,
-                                                      float* __restrict__ cov, int NK, int NKr) {
-    constexpr int SLAB = 64;
-    constexpr int TS = D + 1;
-    __shared__ float tile[SLAB * TS];
-    __shared__ double mu_s[D];
-    const int g = blockIdx.x, bh = blockIdx.y, t = threadIdx.x;
+__global__ __launch_bounds__(256) void moments_partial_kernel(const float* __restrict__ kbar, double* __restrict__ part,
+                                                              int NK, int NKr) {
+    constexpr int SLAB = 32;
+    constexpr int TS = D + 4;                  // f32 row stride of the staged slab
+    constexpr int RB = D / 16;                 // 16x16 thread grid, RB x RB entries each
+    __shared__ float x[SLAB * TS];
+    __shared__ float k0[D];
+    const int sp = blockIdx.x, bh = blockIdx.y, t = threadIdx.x;
     const float* kb = kbar + (size_t)bh * NK * D;
-
-    // pass 1: mean
-    double colsum = 0.0;
-    for (int j0 = 0; j0 < NKr; j0 += SLAB) {
-        const int rows = min(SLAB, NKr - j0);
-        for (int e = t; e < rows * D; e += 256) tile[(e / D) * TS + e % D] = kb[(size_t)(j0 + e / D) * D + e % D];
-        __syncthreads();
-        if (t < D)
-            for (int r = 0; r < rows; ++r) colsum += (double)tile[r * TS + t];
-        __syncthreads();
-    }
-    if (t < D) mu_s[t] = colsum / (double)NKr;
+    const int j0 = (int)((long long)NKr * sp / kMomSplit), j1 = (int)((long long)NKr * (sp + 1) / kMomSplit);
+    for (int c = t; c < D; c += 256) k0[c] = kb[c];
     __syncthreads();
-    if (g == 0 && t < D) muk[(size_t)bh * D + t] = (float)mu_s[t];
-
-    // pass 2: centred second moment, rows [16g, 16g+16)
-    constexpr int CPT = D / 16;  // columns per thread
-    const int r = 16 * g + t / 16, c0 = (t % 16) * CPT;
-    double acc[CPT];
+    const int r0 = (t / 16) * RB, c0 = (t % 16) * RB;
+    double s2[RB][RB];
+    double s1 = 0.0;
 #pragma unroll
-    for (int e = 0; e < CPT; ++e) acc[e] = 0.0;
-    for (int j0 = 0; j0 < NKr; j0 += SLAB) {
-        const int rows = min(SLAB, NKr - j0);
-        for (int e = t; e < rows * D; e += 256)
-            tile[(e / D) * TS + e % D] = (float)((double)kb[(size_t)(j0 + e / D) * D + e % D] - mu_s[e % D]);
+    for (int u = 0; u < RB; ++u)
+#pragma unroll
+        for (int v = 0; v < RB; ++v) s2[u][v] = 0.0;
+    for (int jb = j0; jb < j1; jb += SLAB) {
+        const int rows = min(SLAB, j1 - jb);
+        for (int e = t; e < rows * D; e += 256) x[(e / D) * TS + e % D] = kb[(size_t)(jb + e / D) * D + e % D] - k0[e % D];
         __syncthreads();
         for (int jj = 0; jj < rows; ++jj) {
-            const double a = tile[jj * TS + r];
+            double xr[RB], xc[RB];
 #pragma unroll
-            for (int e = 0; e < CPT; ++e) acc[e] += a * (double)tile[jj * TS + c0 + e];
+            for (int u = 0; u < RB; ++u) {
+                xr[u] = x[jj * TS + r0 + u];
+                xc[u] = x[jj * TS + c0 + u];
+            }
+#pragma unroll
+            for (int u = 0; u < RB; ++u)
+#pragma unroll
+                for (int v = 0; v < RB; ++v) s2[u][v] = fma(xr[u], xc[v], s2[u][v]);
+            if (t < D) s1 += (double)x[jj * TS + t];
         }
         __syncthreads();
     }
+    double* out = part + ((size_t)bh * kMomSplit + sp) * (D * D + D);
 #pragma unroll
-    for (int e = 0; e < CPT; ++e) cov[((size_t)bh * D + r) * D + c0 + e] = (float)(acc[e] / (double)NKr);
+    for (int u = 0; u < RB; ++u)
+#pragma unroll
+        for (int v = 0; v < RB; ++v) out[(r0 + u) * D + c0 + v] = s2[u][v];
+    if (t < D) out[D * D + t] = s1;
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void moments_final_kernel(const float* __restrict__ kbar, const double* __restrict__ part,
+                                                            float* __restrict__ muk, float* __restrict__ cov, int NK,
+                                                            int NKr) {
+    __shared__ double m[D];
+    const int bh = blockIdx.x, t = threadIdx.x;
+    const double* pp = part + (size_t)bh * kMomSplit * (D * D + D);
+    const double inv = 1.0 / (double)NKr;
+    if (t < D) {
+        double s = 0.0;
+        for (int sp = 0; sp < kMomSplit; ++sp) s += pp[(size_t)sp * (D * D + D) + D * D + t];
+        m[t] = s * inv;
+        muk[(size_t)bh * D + t] = (float)((double)kbar[(size_t)bh * NK * D + t] + m[t]);
+    }
+    __syncthreads();
+    for (int e = t; e < D * D; e += 256) {
+        double s = 0.0;
+        for (int sp = 0; sp < kMomSplit; ++sp) s += pp[(size_t)sp * (D * D + D) + e];
+        cov[(size_t)bh * D * D + e] = (float)(s * inv - m[e / D] * m[e % D]);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -508,10 +535,14 @@ struct AttnArgs {
     float bias_full, bias_last;   // log2(n_j)/c_log2 for full blocks and for the last block
 };
 
-// LDS tiles of the fused kernel, without padding.  A K tile is 64 rows x D bf16 (D/8 16-byte
-// chunks per row), a V^T tile is D rows x 64 f16 (8 chunks per row).  Chunk c of row r is
-// stored at chunk position r*CPR + (c ^ (r mod CPR)), so the 16-byte operand reads of 8
-// consecutive rows hit 8 different bank groups.
+// LDS tiles of the fused kernel, without padding.  gfx950 serves a ds_read_b128 16 lanes per
+// cycle from 64 banks, so 16 consecutive MFMA rows reading the same 16-byte chunk column must
+// land on 16 different bank groups.
+//  * K tile (64 rows x D bf16, KCPR = D/8 chunks per row): for D = 128 chunk c of row r sits at
+//    position r*16 + (c ^ (r mod 16)); for D = 64 rows pair into super-rows as below.
+//  * V^T tile (D rows x 64 f16, 8 chunks per row): rows 2R and 2R+1 form a 16-chunk super-row R;
+//    chunk c of row r is super-chunk C = c + 8*(r&1), stored at R*16 + (C ^ (R mod 16)).
+// ksrc()/vsrc() invert the maps for the copy side: LDS chunk position -> (row, chunk).
 template <int D>
 struct TileLds {
     static constexpr int KCPR = D / 8;
@@ -519,8 +550,33 @@ struct TileLds {
     static constexpr int KBYTES = kBlockK * D * 2;
     static constexpr int VBYTES = D * kBlockK * 2;
     static constexpr int STAGE = KBYTES + VBYTES;
-    __device__ static int kpos(int r, int c) { return r * KCPR + (c ^ (r & (KCPR - 1))); }
-    __device__ static int vpos(int r, int c) { return r * VCPR + (c ^ (r & (VCPR - 1))); }
+    // 16-chunk rows (D = 128): XOR with 4 row bits; 8-chunk rows (D = 64): super-rows as for V^T
+    __device__ static int kpos(int r, int c) {
+        if constexpr (KCPR == 16) return r * 16 + (c ^ (r & 15));
+        const int R = r >> 1;
+        return R * 16 + ((c + 8 * (r & 1)) ^ (R & 15));
+    }
+    __device__ static void ksrc(int p, int& r, int& c) {
+        const int R = p >> 4;
+        const int C = (p & 15) ^ (R & 15);
+        if constexpr (KCPR == 16) {
+            r = R;
+            c = C;
+        } else {
+            r = 2 * R + (C >> 3);
+            c = C & 7;
+        }
+    }
+    __device__ static int vpos(int r, int c) {
+        const int R = r >> 1;
+        return R * 16 + ((c + 8 * (r & 1)) ^ (R & 15));
+    }
+    __device__ static void vsrc(int p, int& r, int& c) {
+        const int R = p >> 4;
+        const int C = (p & 15) ^ (R & 15);
+        r = 2 * R + (C >> 3);
+        c = C & 7;
+    }
 };
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
@@ -584,14 +640,14 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     uint32_t koff[KPW], voff[VPW];
 #pragma unroll
     for (int u = 0; u < KPW; ++u) {
-        const int r = ((wave * KPW + u) * 64 + lane) / L::KCPR;
-        const int c = (lane % L::KCPR) ^ (r & (L::KCPR - 1));
+        int r, c;
+        L::ksrc((wave * KPW + u) * 64 + lane, r, c);
         koff[u] = (uint32_t)(r * D + c * 8) * 2u;
     }
 #pragma unroll
     for (int u = 0; u < VPW; ++u) {
-        const int r = ((wave * VPW + u) * 64 + lane) / L::VCPR;
-        const int c = (lane % L::VCPR) ^ (r & (L::VCPR - 1));
+        int r, c;
+        L::vsrc((wave * VPW + u) * 64 + lane, r, c);
         voff[u] = (uint32_t)(r * a.Npad + c * 8) * 2u;
     }
     // Copies of a correction tile (pooled keys of chunk c and their value means) ...
@@ -605,8 +661,8 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
                                              16, 0, 0);
 #pragma unroll
         for (int u = 0; u < VPW; ++u) {
-            const int r = ((wave * VPW + u) * 64 + lane) / L::VCPR;
-            const int c = (lane % L::VCPR) ^ (r & (L::VCPR - 1));
+            int r, c;
+            L::vsrc((wave * VPW + u) * 64 + lane, r, c);
             const uint32_t off = (uint32_t)(r * kChunk + c * 8) * 2u;
             __builtin_amdgcn_global_load_lds((const void*)(vp + off),
                                              (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024), 16, 0, 0);
@@ -625,8 +681,8 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
         } else {
 #pragma unroll
             for (int u = 0; u < KPW; ++u) {
-                const int r = ((wave * KPW + u) * 64 + lane) / L::KCPR;
-                const int c = (lane % L::KCPR) ^ (r & (L::KCPR - 1));
+                int r, c;
+                L::ksrc((wave * KPW + u) * 64 + lane, r, c);
                 const uint32_t off = (uint32_t)(min(r, nrows - 1) * D + c * 8) * 2u;
                 __builtin_amdgcn_global_load_lds((const void*)(kp + off), (lds_ptr_t)(stage + (wave * KPW + u) * 1024),
                                                  16, 0, 0);
@@ -767,11 +823,12 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
         constexpr int SOFF = decltype(stage_tag)::value * L::STAGE;
         f16x8 av[2];
         av[0] = *reinterpret_cast<const f16x8*>(smem + vadr[0] + SOFF);
+        // kk-major: consecutive MFMAs update different accumulators (no dependent issue)
 #pragma unroll
         for (int i = 0; i < NDT * 4; ++i) {
-            const int mt = i >> 2, kk = i & 3;
+            const int kk = i / NDT, mt = i % NDT;
             if (i + 1 < NDT * 4) {
-                const int mt1 = (i + 1) >> 2, kk1 = (i + 1) & 3;
+                const int kk1 = (i + 1) / NDT, mt1 = (i + 1) % NDT;
                 av[(i + 1) & 1] = *reinterpret_cast<const f16x8*>(smem + vadr[kk1] + SOFF + mt1 * VMT);
             }
             o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i & 1], pb[kk], o[mt], 0, 0, 0);
@@ -834,7 +891,13 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
         qk(EXACT_T{}, S0{}, qf, s0, s1);
         float mx = tile_max(s0, s1);
         // iteration t with t & 1 == P: K of tile t+1 in stage P^1, V of tile t in stage P
-        auto step = [&](auto par_tag, int t) {
+        // D = 128: one pipelined iteration as 32 MFMA slots.  Slots 0-3 run QK^T of tile t+1
+        // while the exponentials of P block 0 of tile t are formed; three blocks of 8 slots then
+        // alternate QK^T(t+1) and PV(t) while the next P block is formed; the last 4 slots are
+        // PV only, overlapped with the row max of tile t+1.  Successive MFMAs on one accumulator
+        // are at least two slots apart, and operands are read from LDS two slots ahead.
+        // Generic iteration (any D): the same work in source order.
+        auto step_generic = [&](auto par_tag, int t) {
             constexpr int P = decltype(par_tag)::value;
             rescale(mx);
             if (t + 2 < T) issue_exact_k(ecode(t + 2), P);
@@ -849,6 +912,80 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
             __syncthreads();
             s0 = n0;
             s1 = n1;
+        };
+        auto step_slots = [&](auto par_tag, int t) {
+            constexpr int P = decltype(par_tag)::value;
+            constexpr int KOFF = (P ^ 1) * L::STAGE;   // K of tile t+1
+            constexpr int VOFF = P * L::STAGE;         // V of tile t
+            rescale(mx);
+            if (t + 2 < T) issue_exact_k(ecode(t + 2), P);
+            issue_exact_v(ecode(t + 1), P ^ 1);
+            const float msub = m_run == kNegInf ? 0.f : m_run;
+            const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
+            f16x8 pb[4];
+            auto exp_pair = [&](int kk, int q) {        // elements 2q, 2q+1 of P block kk
+                const int tt = kk >> 1, r = 8 * (kk & 1) + 2 * q;
+                const float x0 = tt ? s1[r] : s0[r];
+                const float x1 = tt ? s1[r + 1] : s0[r + 1];
+                const float p0 = __builtin_amdgcn_exp2f(fmaf(x0, cl, -msub));
+                const float p1 = __builtin_amdgcn_exp2f(fmaf(x1, cl, -msub));
+                const f16x2 pp = {(_Float16)p0, (_Float16)p1};
+                l_run = __builtin_amdgcn_fdot2(pp, ones, l_run, false);
+                pb[kk][2 * q] = pp[0];
+                pb[kk][2 * q + 1] = pp[1];
+            };
+            // slot -> operation: kind 0 = QK (index qi: ks = qi/2, half = qi%2), 1 = PV (pi: kk = pi/4)
+            auto kind = [](int sl) { return sl < 4 ? 0 : (sl < 28 ? ((sl - 4) & 1) : 1); };
+            auto index = [](int sl) {
+                if (sl < 4) return sl;
+                if (sl < 28) {
+                    const int u = sl - 4, b = u >> 3, w = u & 7;
+                    return (w & 1) ? 4 * b + (w >> 1) : 4 + 4 * b + (w >> 1);
+                }
+                return 12 + (sl - 28);
+            };
+            auto ldk = [&](int qi) {
+                return *reinterpret_cast<const bf16x8*>(smem + kadr[qi >> 1] + KOFF + (qi & 1) * KT1);
+            };
+            auto ldv = [&](int pi) {
+                return *reinterpret_cast<const f16x8*>(smem + vadr[pi >> 2] + VOFF + (pi & 3) * VMT);
+            };
+            bf16x8 kop[4];
+            f16x8 vop[4];
+            int nk = 0, nv = 0;   // operands loaded so far (ring of 4)
+            auto prefetch = [&](int sl) {
+                if (sl >= 32) return;
+                if (kind(sl) == 0) kop[(nk++) & 3] = ldk(index(sl));
+                else vop[(nv++) & 3] = ldv(index(sl));
+            };
+            f32x16 n0 = f32x16{}, n1 = f32x16{};
+            prefetch(0);
+            prefetch(1);
+            int ck = 0, cv = 0;   // operands consumed so far
+#pragma unroll
+            for (int sl = 0; sl < 32; ++sl) {
+                prefetch(sl + 2);
+                const int id = index(sl);
+                if (kind(sl) == 0) {
+                    const bf16x8 av = kop[(ck++) & 3];
+                    if (id & 1) n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[id >> 1], n1, 0, 0, 0);
+                    else n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[id >> 1], n0, 0, 0, 0);
+                } else {
+                    const f16x8 av = vop[(cv++) & 3];
+                    o[id & 3] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, pb[id >> 2], o[id & 3], 0, 0, 0);
+                }
+                if (sl < 4) exp_pair(0, sl);
+                else if (sl < 28 && !((sl - 4) & 1)) exp_pair(((sl - 4) >> 3) + 1, ((sl - 4) & 7) >> 1);
+            }
+            mx = tile_max(n0, n1);
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+            s0 = n0;
+            s1 = n1;
+        };
+        auto step = [&](auto par_tag, int t) {
+            if constexpr (D == 128) step_slots(par_tag, t);
+            else step_generic(par_tag, t);
         };
         int t = 0;
         for (; t + 2 < T; t += 2) {
@@ -1106,6 +1243,7 @@ size_t workspace_layout(const Shape& s, char* base, Workspace* ws) {
         w.muk = reinterpret_cast<float*>(take(BH * d * 4));
         w.cov = reinterpret_cast<float*>(take(BH * d * d * 4));
         w.tau = reinterpret_cast<float*>(take(BH * s.NQ * 4));
+        w.mom = reinterpret_cast<double*>(take(moments_scratch_bytes(s.BH, s.d)));
     }
     if (s.dtype == kBF16) {
         w.vt = reinterpret_cast<_Float16*>(take(BH * d * (size_t)s.Npad * 2));
@@ -1130,9 +1268,17 @@ hipError_t launch_pool_mean(const void* x, float* mean, int dtype, int BH, int N
     return hipGetLastError();
 }
 
-hipError_t launch_moments(const float* kbar, float* muk, float* cov, int BH, int NK, int NKr, int d, hipStream_t st) {
-    if (d == 128) moments_kernel<128><<<dim3(128 / 16, BH), dim3(256), 0, st>>>(kbar, muk, cov, NK, NKr);
-    else moments_kernel<64><<<dim3(64 / 16, BH), dim3(256), 0, st>>>(kbar, muk, cov, NK, NKr);
+size_t moments_scratch_bytes(int BH, int d) { return (size_t)BH * kMomSplit * ((size_t)d * d + d) * sizeof(double); }
+
+hipError_t launch_moments(const float* kbar, float* muk, float* cov, double* scratch, int BH, int NK, int NKr, int d,
+                          hipStream_t st) {
+    if (d == 128) {
+        moments_partial_kernel<128><<<dim3(kMomSplit, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr);
+        moments_final_kernel<128><<<dim3(BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr);
+    } else {
+        moments_partial_kernel<64><<<dim3(kMomSplit, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr);
+        moments_final_kernel<64><<<dim3(BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr);
+    }
     return hipGetLastError();
 }
 
@@ -1176,7 +1322,7 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
                                                                      s.NK, s.NKr, s.NC, s.Npad, routing ? 1 : 0);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (routing) {
-            if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, s.BH, s.NK, s.NKr, d, st)) != hipSuccess) return e;
+            if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, ws.mom, s.BH, s.NK, s.NKr, d, st)) != hipSuccess) return e;
             if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, st)) != hipSuccess)
                 return e;
         }
@@ -1209,7 +1355,7 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
             if ((e = launch_pool_mean(k, ws.kbar, kF32, s.BH, s.N, d, s.bk, st)) != hipSuccess) return e;
             if (s.mode == kSparse && (e = launch_pool_mean(v, ws.vbar, kF32, s.BH, s.N, d, s.bk, st)) != hipSuccess)
                 return e;
-            if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, s.BH, s.NK, s.NKr, d, st)) != hipSuccess) return e;
+            if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, ws.mom, s.BH, s.NK, s.NKr, d, st)) != hipSuccess) return e;
             if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, st)) != hipSuccess)
                 return e;
         }
