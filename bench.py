@@ -73,24 +73,43 @@ def measured_traffic(workload, kept):
 
 
 def time_steps(fn, steps, warmup):
+    """Mean step time over exactly `steps` steps bracketed by device synchronisation, plus
+    the median and interquartile range of the per-step times (events around each step on the
+    launch stream) and the mean duration of the fused attention kernel (HIP events recorded
+    by the library around each launch)."""
     import torch
     from paper_2607_24027_amd import binding
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
     binding.timing_enable(True)
-    t0 = torch.cuda.Event(enable_timing=True)
-    t1 = torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
-    t0.record()
-    for _ in range(steps):
+    ev[0].record()
+    for i in range(steps):
         fn()
-    t1.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
-    total = t0.elapsed_time(t1)
+    total = ev[0].elapsed_time(ev[-1])
+    per = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(steps)])
     kms, n = binding.kernel_timing()
     binding.timing_enable(False)
-    return total / steps, kms / max(n, 1)
+    q1, med, q3 = np.percentile(per, [25, 50, 75])
+    return {"mean": total / steps, "median": float(med), "iqr": float(q3 - q1), "kernel": kms / max(n, 1)}
+
+
+def band_count(qd, kd, vd, w, beta):
+    """Routable pairs whose proxy lies within 1e-3 of the row threshold (reporting only; the
+    pooled means and thresholds come from the library, the proxies from an f64 matmul)."""
+    import torch
+    from paper_2607_24027_amd import binding
+    if not math.isfinite(beta):
+        return 0
+    nkr = w.NK - w.text_tokens // w.block_k
+    qbar, kbar, _ = binding.pool_blocks(qd, kd, vd, w.block_q, w.block_k)
+    tau, _, _ = binding.thresholds(qbar, kbar, beta, nkr)
+    s_hat = torch.matmul(qbar.double(), kbar[:, :, :nkr].double().transpose(-1, -2).contiguous()) / math.sqrt(w.d)
+    return int((s_hat - tau.double()[..., None]).abs().lt(1e-3).sum().item())
 
 
 def cpu_baseline(w, q, k, v, beta, seconds):
@@ -123,8 +142,8 @@ def cpu_baseline(w, q, k, v, beta, seconds):
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="video720p")
     ap.add_argument("--kept", type=float, default=None, help="kept fraction (a calibrated sweep point)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -174,17 +193,20 @@ def main():
         return lambda: binding.forward(qd, kd, vd, w.block_q, w.block_k, b, mode, keep, out=out)
 
     log("timing sparse")
-    sp_ms, sp_kernel_ms = time_steps(step("sparse", beta), args.steps, args.warmup)
+    sp = time_steps(step("sparse", beta), args.steps, args.warmup)
     stats = binding.stats(w.B, w.H)
     log("timing sparse_no_correction")
-    nc_ms, nc_kernel_ms = time_steps(step("sparse_no_correction", beta), args.steps, args.warmup)
+    nc = time_steps(step("sparse_no_correction", beta), args.steps, args.warmup)
     log("timing dense")
-    dn_ms, dn_kernel_ms = time_steps(step("dense", beta), args.steps, args.warmup)
+    dn = time_steps(step("dense", beta), args.steps, args.warmup)
+    band = band_count(qd, kd, vd, w, beta)
 
+    sp_ms, dn_ms = sp["mean"], dn["mean"]
     dense_flop = w.dense_flop
     value = dense_flop / (sp_ms * 1e-3) / 1e12
-    achieved = (exact_flop + approx_flop) / (sp_kernel_ms * 1e-3) / 1e12
-    dense_achieved = dense_flop / (dn_kernel_ms * 1e-3) / 1e12
+    achieved = (exact_flop + approx_flop) / (sp["kernel"] * 1e-3) / 1e12
+    dense_achieved = dense_flop / (dn["kernel"] * 1e-3) / 1e12
+    r4 = lambda x: round(x, 4)
     res = {
         "metric": "dense-equiv attention TFLOP/s + speedup vs dense @720p-shape bf16, 1 MI355X",
         "value": round(value, 3),
@@ -192,7 +214,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(sp_ms, 4),
+        "ms_per_step": r4(sp_ms),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -201,19 +223,23 @@ def main():
         "config": {"workload": w.name, "B": w.B, "H": w.H, "N": w.N, "d": w.d, "block_q": w.block_q,
                    "block_k": w.block_k, "text_tokens": w.text_tokens, "kept_target": kept,
                    "beta": beta, "mode": "sparse"},
-        "speedup_vs_dense": round(dn_ms / sp_ms, 4),
-        "target_speedup": round(0.8 / float(frac.mean()), 4),
+        "speedup_vs_dense": r4(dn_ms / sp_ms),
+        "speedup_vs_dense_kernel": r4(dn["kernel"] / sp["kernel"]),
+        "target_speedup": r4(0.8 / float(frac.mean())),
         "selected_fraction": {"mean": float(frac.mean()), "min": float(frac.min()), "max": float(frac.max()),
                               "from_counts_mean": float(np.mean(stats))},
-        "dense_ms_per_step": round(dn_ms, 4),
-        "sparse_no_correction_ms_per_step": round(nc_ms, 4),
-        "correction_overhead": round(sp_ms / nc_ms - 1.0, 4),
-        "attn_kernel_ms": {"sparse": round(sp_kernel_ms, 4), "sparse_no_correction": round(nc_kernel_ms, 4),
-                           "dense": round(dn_kernel_ms, 4)},
-        "mfma_util_computed_tiles": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
-        "dense_mode_mfma_util": round(dense_achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+        "band_pairs": band,
+        "step_ms": {"sparse": {"mean": r4(sp_ms), "median": r4(sp["median"]), "iqr": r4(sp["iqr"])},
+                    "sparse_no_correction": {"mean": r4(nc["mean"]), "median": r4(nc["median"]),
+                                             "iqr": r4(nc["iqr"])},
+                    "dense": {"mean": r4(dn_ms), "median": r4(dn["median"]), "iqr": r4(dn["iqr"])}},
+        "attn_kernel_ms": {"sparse": r4(sp["kernel"]), "sparse_no_correction": r4(nc["kernel"]),
+                           "dense": r4(dn["kernel"])},
+        "correction_overhead": r4(sp_ms / nc["mean"] - 1.0),
+        "mfma_util_computed_tiles": r4(achieved / MFMA_BF16_PEAK_TFLOPS),
+        "dense_mode_mfma_util": r4(dense_achieved / MFMA_BF16_PEAK_TFLOPS),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": MFMA_BF16_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "unit": "TFLOP/s", "frac": r4(achieved / MFMA_BF16_PEAK_TFLOPS),
                      "traffic": measured_traffic(w.name, kept),
                      "kernel": "routed_attn_kernel<128,128,sparse>",
                      "flop_per_launch": exact_flop + approx_flop, "exact_flop": exact_flop,

@@ -237,6 +237,10 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict
 // ---------------------------------------------------------------------------
 constexpr int kMomSplit = 8;
 
+// Device lambdas of the attention kernel are always inlined: a call would move the register
+// tile state through memory.
+#define SOL_INLINE __attribute__((always_inline))
+
 template <int D>
 __global__ __launch_bounds__(256) void moments_partial_kernel(const float* __restrict__ kbar, double* __restrict__ part,
                                                               int NK, int NKr) {
@@ -581,8 +585,26 @@ struct TileLds {
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
+// Direct global->LDS copy of 16 bytes per lane (LDS bytes [dst + 16*lane, +16)), written as
+// inline assembly so that the compiler's wait-count model does not track it: the exact-tile
+// loop orders its copies with its own s_waitcnt/barrier pairs, and the compiler, which would
+// otherwise treat every later LDS read as possibly aliasing an in-flight copy, is left free
+// to schedule the operand reads.  dst must be wave-uniform (it goes to m0); the s_nop covers
+// the one-wait-state hazard between an m0 write and an LDS DMA that reads it.
+__device__ __forceinline__ void lds_copy16(const void* src, lds_ptr_t dst) {
+    const uint32_t m0 = (uint32_t)(uintptr_t)dst;
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(m0) : "memory");
+}
+
+// Waves per SIMD the attention kernel is register-budgeted for: two, except where the LDS of a
+// workgroup (two 32 KB tile stages for d = 128) leaves room for only four waves per CU, i.e.
+// two-wave workgroups at d = 128, which then get the full register file.
+template <int D, int BQ>
+constexpr int kAttnWavesPerEU = (D == 128 && BQ == 64) ? 1 : 2;
+
 template <int D, int BQ, int MODE>
-__global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) void routed_attn_kernel(AttnArgs a) {
+__global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(kAttnWavesPerEU<D, BQ>, kAttnWavesPerEU<D, BQ>)))
+void routed_attn_kernel(AttnArgs a) {
     constexpr int NT = BQ * 2;            // 64 threads per 32 query rows
     constexpr int NW = NT / 64;
     using L = TileLds<D>;
@@ -636,67 +658,79 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     // byte offsets inside a tile are fixed, so they are computed once here and each tile only
     // adds wave-uniform base pointers.  Rows past the end of the sequence (ragged last block)
     // are clamped to the last valid row: their scores are masked to -inf and their values
-    // are zero in V^T.
-    uint32_t koff[KPW], voff[VPW];
-#pragma unroll
-    for (int u = 0; u < KPW; ++u) {
+    // are zero in V^T.  Two-wave workgroups issue twice as many copies per wave and recompute
+    // the offsets instead of holding them in registers.
+    constexpr bool kKeepOff = NW >= 4;
+    auto kofs_calc = [&](int u) SOL_INLINE -> uint32_t {
         int r, c;
         L::ksrc((wave * KPW + u) * 64 + lane, r, c);
-        koff[u] = (uint32_t)(r * D + c * 8) * 2u;
-    }
-#pragma unroll
-    for (int u = 0; u < VPW; ++u) {
+        return (uint32_t)(r * D + c * 8) * 2u;
+    };
+    auto vofs_calc = [&](int u) SOL_INLINE -> uint32_t {
         int r, c;
         L::vsrc((wave * VPW + u) * 64 + lane, r, c);
-        voff[u] = (uint32_t)(r * a.Npad + c * 8) * 2u;
+        return (uint32_t)(r * a.Npad + c * 8) * 2u;
+    };
+    uint32_t koff[kKeepOff ? KPW : 1], voff[kKeepOff ? VPW : 1];
+    if constexpr (kKeepOff) {
+#pragma unroll
+        for (int u = 0; u < KPW; ++u) koff[u] = kofs_calc(u);
+#pragma unroll
+        for (int u = 0; u < VPW; ++u) voff[u] = vofs_calc(u);
     }
-    // Copies of a correction tile (pooled keys of chunk c and their value means) ...
-    auto issue_apx = [&](int c, int buf) {
+    auto kofs = [&](int u) SOL_INLINE -> uint32_t {
+        if constexpr (kKeepOff) return koff[u];
+        else return kofs_calc(u);
+    };
+    auto vofs = [&](int u) SOL_INLINE -> uint32_t {
+        if constexpr (kKeepOff) return voff[u];
+        else return vofs_calc(u);
+    };
+    // Copies of a correction tile: the f16 pooled keys of chunk c into stage `buf`'s K region ...
+    auto issue_apx_k = [&](int c, int buf) SOL_INLINE {
         char* stage = smem + buf * L::STAGE;
         const char* kp = reinterpret_cast<const char*>(a.kbarh + ((size_t)bh * a.NC * kChunk + (size_t)c * kChunk) * D);
+#pragma unroll
+        for (int u = 0; u < KPW; ++u) lds_copy16(kp + kofs(u), (lds_ptr_t)(stage + (wave * KPW + u) * 1024));
+    };
+    // ... and their transposed f16 value means into its V region ...
+    auto issue_apx_v = [&](int c, int buf) SOL_INLINE {
+        char* stage = smem + buf * L::STAGE;
         const char* vp = reinterpret_cast<const char*>(a.vbart + ((size_t)bh * a.NC + c) * D * kChunk);
 #pragma unroll
-        for (int u = 0; u < KPW; ++u)
-            __builtin_amdgcn_global_load_lds((const void*)(kp + koff[u]), (lds_ptr_t)(stage + (wave * KPW + u) * 1024),
-                                             16, 0, 0);
-#pragma unroll
         for (int u = 0; u < VPW; ++u) {
-            int r, c;
-            L::vsrc((wave * VPW + u) * 64 + lane, r, c);
-            const uint32_t off = (uint32_t)(r * kChunk + c * 8) * 2u;
-            __builtin_amdgcn_global_load_lds((const void*)(vp + off),
-                                             (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024), 16, 0, 0);
+            int r, cc;
+            L::vsrc((wave * VPW + u) * 64 + lane, r, cc);
+            const uint32_t off = (uint32_t)(r * kChunk + cc * 8) * 2u;
+            lds_copy16(vp + off, (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024));
         }
     };
     // ... and of an exact tile: key block j into stage `buf`'s K region ...
-    auto issue_exact_k = [&](int j, int buf) {
+    auto issue_exact_k = [&](int j, int buf) SOL_INLINE {
         char* stage = smem + buf * L::STAGE;
         const char* kp = reinterpret_cast<const char*>(a.k + ((size_t)bh * a.N + (size_t)j * kBlockK) * D);
         const int nrows = a.N - j * kBlockK;
         if (nrows >= kBlockK) {
 #pragma unroll
             for (int u = 0; u < KPW; ++u)
-                __builtin_amdgcn_global_load_lds((const void*)(kp + koff[u]),
-                                                 (lds_ptr_t)(stage + (wave * KPW + u) * 1024), 16, 0, 0);
+                lds_copy16(kp + kofs(u), (lds_ptr_t)(stage + (wave * KPW + u) * 1024));
         } else {
 #pragma unroll
             for (int u = 0; u < KPW; ++u) {
                 int r, c;
                 L::ksrc((wave * KPW + u) * 64 + lane, r, c);
                 const uint32_t off = (uint32_t)(min(r, nrows - 1) * D + c * 8) * 2u;
-                __builtin_amdgcn_global_load_lds((const void*)(kp + off), (lds_ptr_t)(stage + (wave * KPW + u) * 1024),
-                                                 16, 0, 0);
+                lds_copy16(kp + off, (lds_ptr_t)(stage + (wave * KPW + u) * 1024));
             }
         }
     };
     // ... and its transposed values into stage `buf`'s V region.
-    auto issue_exact_v = [&](int j, int buf) {
+    auto issue_exact_v = [&](int j, int buf) SOL_INLINE {
         char* stage = smem + buf * L::STAGE;
         const char* vp = reinterpret_cast<const char*>(a.vt + (size_t)bh * D * a.Npad + (size_t)j * kBlockK);
 #pragma unroll
         for (int u = 0; u < VPW; ++u)
-            __builtin_amdgcn_global_load_lds((const void*)(vp + voff[u]),
-                                             (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024), 16, 0, 0);
+            lds_copy16(vp + vofs(u), (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024));
     };
 
     const float cl = a.c_log2;
@@ -717,7 +751,7 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     // S^T = K Q^T over two 32-key M-tiles, operands double-buffered in registers.  Exact
     // tiles: bf16 keys x bf16 queries.  Correction tiles: f16 pooled keys x f16 queries, so the
     // pooled keys keep 11 significant bits.
-    auto qk = [&](auto apx_tag, auto stage_tag, const auto& qop, f32x16& s0, f32x16& s1) {
+    auto qk = [&](auto apx_tag, auto stage_tag, const auto& qop, f32x16& s0, f32x16& s1) SOL_INLINE {
         constexpr bool APX = decltype(apx_tag)::value;
         constexpr int SOFF = decltype(stage_tag)::value * L::STAGE;
         using AT = std::conditional_t<APX, f16x8, bf16x8>;
@@ -740,7 +774,7 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
         }
     };
     // Keys past the end of the sequence (only in the last key block) -> -inf.
-    auto mask_tail = [&](int j, f32x16& s0, f32x16& s1) {
+    auto mask_tail = [&](int j, f32x16& s0, f32x16& s1) SOL_INLINE {
         const int nvalid = a.N - j * kBlockK;
         if (nvalid < kBlockK) {
 #pragma unroll
@@ -753,20 +787,24 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     };
     // Correction tile of chunk c: slot j contributes with log2(n_j) (the multiplicity of Eq.
     // solattn_denominator) unless it is selected (exact tile) or past the routable keys.
-    auto bias_apx = [&](int c, f32x16& s0, f32x16& s1) {
-        const uint32_t wlo = selw[2 * c];
-        const uint32_t whi = 2 * c + 1 < a.MW ? selw[2 * c + 1] : 0u;
+    auto bias_apx = [&](int c, f32x16& s0, f32x16& s1) SOL_INLINE {
+        // Element r of this lane's score registers holds slot 4*hh + off(r) (s0) or 32 + that
+        // (s1), off(r) = 8*(r/4) + r%4.  Per slot half, one word marks the slots that take the
+        // bias (valid and unselected); shifting it by 4*hh leaves compile-time bit positions.
         const int nvalid = min(kChunk, a.NKr - c * kChunk);
-        const int last_slot = a.NK - 1 - c * kChunk;   // slot of the (possibly short) last block
-        auto apx_bias = [&](int slot, uint32_t word) -> float {
-            const bool ok = slot < nvalid && !((word >> (slot & 31)) & 1u);
-            return ok ? (slot == last_slot ? a.bias_last : a.bias_full) : kNegInf;
-        };
+        const uint32_t vlo = nvalid >= 32 ? 0xffffffffu : (nvalid <= 0 ? 0u : ((1u << nvalid) - 1u));
+        const uint32_t vhi = nvalid >= 64 ? 0xffffffffu : (nvalid <= 32 ? 0u : ((1u << (nvalid - 32)) - 1u));
+        const uint32_t whi = 2 * c + 1 < a.MW ? selw[2 * c + 1] : 0u;
+        const uint32_t blo = (~selw[2 * c] & vlo) >> (4 * hh);
+        const uint32_t bhi = (~whi & vhi) >> (4 * hh);
+        const int last = a.NK - 1 - c * kChunk - 4 * hh;   // off() of the (possibly short) last block
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-            const int slot0 = 8 * (r >> 2) + 4 * hh + (r & 3);
-            s0[r] += apx_bias(slot0, wlo);
-            s1[r] += apx_bias(32 + slot0, whi);
+            const int off = 8 * (r >> 2) + (r & 3);
+            const float b0 = (off == last) ? a.bias_last : a.bias_full;
+            const float b1 = (off + 32 == last) ? a.bias_last : a.bias_full;
+            s0[r] += ((blo >> off) & 1u) ? b0 : kNegInf;
+            s1[r] += ((bhi >> off) & 1u) ? b1 : kNegInf;
         }
     };
     // Online softmax in the log2 domain with lazy rescaling, split so that the (rarely
@@ -774,13 +812,13 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     //   tile_max  - row max of a score tile (both lane halves of a query agree)
     //   rescale   - raise the running max if a tile exceeds it by more than kRescaleSlack
     //   exps      - P^T = exp2(S*c - m) packed as f16 B operands; row sums from the rounded P
-    auto tile_max = [&](const f32x16& s0, const f32x16& s1) -> float {
+    auto tile_max = [&](const f32x16& s0, const f32x16& s1) SOL_INLINE -> float {
         float mx = kNegInf;
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
         return fmaxf(mx, __shfl_xor(mx, 32));
     };
-    auto rescale = [&](float mx) {
+    auto rescale = [&](float mx) SOL_INLINE {
         const float mt_ = mx * cl;
         const bool need = mt_ > m_run + kRescaleSlack;
         if (__ballot(need)) {
@@ -792,7 +830,7 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
             m_run = mnew;
         }
     };
-    auto exps = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[4]) {
+    auto exps = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[4]) SOL_INLINE {
         const float msub = m_run == kNegInf ? 0.f : m_run;
         const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
 #pragma unroll
@@ -814,12 +852,12 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
             }
         }
     };
-    auto softmax = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[4]) {
+    auto softmax = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[4]) SOL_INLINE {
         rescale(tile_max(s0, s1));
         exps(s0, s1, pb);
     };
     // O^T += V^T P^T, operands double-buffered in registers.
-    auto pv = [&](auto stage_tag, const f16x8 (&pb)[4]) {
+    auto pv = [&](auto stage_tag, const f16x8 (&pb)[4]) SOL_INLINE {
         constexpr int SOFF = decltype(stage_tag)::value * L::STAGE;
         f16x8 av[2];
         av[0] = *reinterpret_cast<const f16x8*>(smem + vadr[0] + SOFF);
@@ -839,56 +877,49 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
     using APX_T = std::integral_constant<bool, true>;
     using EXACT_T = std::integral_constant<bool, false>;
 
-    // ---- correction tiles (sparse mode): one stage per tile, prefetch one tile ahead -------
-    if (MODE == kSparse && napx > 0) {
-        f16x8 qh[NKS];
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks) {
-            const bf16x8 qv = qrow < a.N ? *reinterpret_cast<const bf16x8*>(qrow_p + 16 * ks) : bf16x8{};
-#pragma unroll
-            for (int e = 0; e < 8; ++e) qh[ks][e] = (_Float16)(float)qv[e];
-        }
-        issue_apx(list[0] & ~kApxFlag, 0);
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        auto apx_tile = [&](auto stage_tag, int n) {
-            constexpr int ST = decltype(stage_tag)::value;
-            const int c = list[n] & ~kApxFlag;
-            if (n + 1 < napx) issue_apx(list[n + 1] & ~kApxFlag, ST ^ 1);
-            f32x16 s0 = f32x16{}, s1 = f32x16{};
-            qk(APX_T{}, stage_tag, qh, s0, s1);
-            bias_apx(c, s0, s1);
-            f16x8 pb[4];
-            softmax(s0, s1, pb);
-            pv(stage_tag, pb);
-            __builtin_amdgcn_s_waitcnt(0);
-            __syncthreads();
-        };
-        for (int n = 0; n < napx; n += 2) {
-            apx_tile(S0{}, n);
-            if (n + 1 < napx) apx_tile(S1{}, n + 1);
-        }
-    }
-
-    // ---- exact tiles: software-pipelined, keys one tile ahead of values --------------------
-    // Iteration t computes the scores of tile t+1 (MFMA) while the softmax of tile t (VALU)
+    // ---- tile pipeline -------------------------------------------------------------------
+    // Both kinds of tile run the same software pipeline, keys one tile ahead of values:
+    // iteration t computes the scores of tile t+1 (MFMA) while the softmax of tile t (VALU)
     // runs, then O += V_t P_t.  Stage b's K region holds tile t+1 while its V region still
     // holds tile t, so both stages are busy without a third buffer.  The loop is unrolled by
     // two so that the stage of every LDS access is a compile-time offset.
-    const int T = ntiles - napx;
-    auto ecode = [&](int t) -> int { return tile_code(napx + t); };
-    if (T > 0) {
-        bf16x8 qf[NKS];
-#pragma unroll
-        for (int ks = 0; ks < NKS; ++ks)
-            qf[ks] = qrow < a.N ? *reinterpret_cast<const bf16x8*>(qrow_p + 16 * ks) : bf16x8{};
-        issue_exact_k(ecode(0), 0);
-        issue_exact_v(ecode(0), 0);
-        if (T > 1) issue_exact_k(ecode(1), 1);
+    //   correction tiles (sparse mode, list entries [0, napx)): a chunk of f16 pooled keys
+    //     against the f16 query copy, plus the multiplicity bias of each slot;
+    //   exact tiles (list entries [napx, ntiles)): a bf16 key block against the bf16 queries.
+    // The ragged last key block can only be the final exact tile (it is the last selected or
+    // the last forced block), so its mask is applied after the loop.
+    auto pipeline = [&](auto apx_tag, const auto& qop, const int T, auto code) SOL_INLINE {
+        constexpr bool APX = decltype(apx_tag)::value;
+        using KT = std::conditional_t<APX, f16x8, bf16x8>;
+        auto issue_k = [&](int t, int buf) SOL_INLINE {
+            if constexpr (APX) issue_apx_k(code(t), buf);
+            else issue_exact_k(code(t), buf);
+        };
+        auto issue_v = [&](int t, int buf) SOL_INLINE {
+            if constexpr (APX) issue_apx_v(code(t), buf);
+            else issue_exact_v(code(t), buf);
+        };
+        auto mfma_qk = [](const KT& av, const KT& bq, const f32x16& acc) SOL_INLINE {
+            if constexpr (APX) return __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bq, acc, 0, 0, 0);
+            else return __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bq, acc, 0, 0, 0);
+        };
+        // scores of tile t are complete: add the correction bias (correction tiles)
+        auto scores_done = [&](int t, f32x16& s0, f32x16& s1) SOL_INLINE {
+            if constexpr (APX) {
+                // keep the selection-word reads (and the biases built from them) here rather
+                // than hoisted across the MFMA slots, where they would hold 32 registers
+                asm volatile("" ::: "memory");
+                bias_apx(code(t), s0, s1);
+            }
+        };
+        issue_k(0, 0);
+        issue_v(0, 0);
+        if (T > 1) issue_k(1, 1);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         f32x16 s0 = f32x16{}, s1 = f32x16{};
-        qk(EXACT_T{}, S0{}, qf, s0, s1);
+        qk(apx_tag, S0{}, qop, s0, s1);
+        scores_done(0, s0, s1);
         float mx = tile_max(s0, s1);
         // iteration t with t & 1 == P: K of tile t+1 in stage P^1, V of tile t in stage P
         // D = 128: one pipelined iteration as 32 MFMA slots.  Slots 0-3 run QK^T of tile t+1
@@ -897,33 +928,34 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
         // PV only, overlapped with the row max of tile t+1.  Successive MFMAs on one accumulator
         // are at least two slots apart, and operands are read from LDS two slots ahead.
         // Generic iteration (any D): the same work in source order.
-        auto step_generic = [&](auto par_tag, int t) {
+        auto step_generic = [&](auto par_tag, int t) SOL_INLINE {
             constexpr int P = decltype(par_tag)::value;
             rescale(mx);
-            if (t + 2 < T) issue_exact_k(ecode(t + 2), P);
-            issue_exact_v(ecode(t + 1), P ^ 1);
+            if (t + 2 < T) issue_k(t + 2, P);
+            issue_v(t + 1, P ^ 1);
             f32x16 n0 = f32x16{}, n1 = f32x16{};
-            qk(EXACT_T{}, std::integral_constant<int, P ^ 1>{}, qf, n0, n1);
+            qk(apx_tag, std::integral_constant<int, P ^ 1>{}, qop, n0, n1);
             f16x8 pb[4];
-            exps(s0, s1, pb);         // tile t is never the ragged last block here
+            exps(s0, s1, pb);
             pv(par_tag, pb);
+            scores_done(t + 1, n0, n1);
             mx = tile_max(n0, n1);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             s0 = n0;
             s1 = n1;
         };
-        auto step_slots = [&](auto par_tag, int t) {
+        auto step_slots = [&](auto par_tag, int t) SOL_INLINE {
             constexpr int P = decltype(par_tag)::value;
             constexpr int KOFF = (P ^ 1) * L::STAGE;   // K of tile t+1
             constexpr int VOFF = P * L::STAGE;         // V of tile t
             rescale(mx);
-            if (t + 2 < T) issue_exact_k(ecode(t + 2), P);
-            issue_exact_v(ecode(t + 1), P ^ 1);
+            if (t + 2 < T) issue_k(t + 2, P);
+            issue_v(t + 1, P ^ 1);
             const float msub = m_run == kNegInf ? 0.f : m_run;
             const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
             f16x8 pb[4];
-            auto exp_pair = [&](int kk, int q) {        // elements 2q, 2q+1 of P block kk
+            auto exp_pair = [&](int kk, int q) SOL_INLINE {   // elements 2q, 2q+1 of P block kk
                 const int tt = kk >> 1, r = 8 * (kk & 1) + 2 * q;
                 const float x0 = tt ? s1[r] : s0[r];
                 const float x1 = tt ? s1[r + 1] : s0[r + 1];
@@ -935,8 +967,8 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
                 pb[kk][2 * q + 1] = pp[1];
             };
             // slot -> operation: kind 0 = QK (index qi: ks = qi/2, half = qi%2), 1 = PV (pi: kk = pi/4)
-            auto kind = [](int sl) { return sl < 4 ? 0 : (sl < 28 ? ((sl - 4) & 1) : 1); };
-            auto index = [](int sl) {
+            auto kind = [](int sl) SOL_INLINE { return sl < 4 ? 0 : (sl < 28 ? ((sl - 4) & 1) : 1); };
+            auto index = [](int sl) SOL_INLINE {
                 if (sl < 4) return sl;
                 if (sl < 28) {
                     const int u = sl - 4, b = u >> 3, w = u & 7;
@@ -944,16 +976,16 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
                 }
                 return 12 + (sl - 28);
             };
-            auto ldk = [&](int qi) {
-                return *reinterpret_cast<const bf16x8*>(smem + kadr[qi >> 1] + KOFF + (qi & 1) * KT1);
+            auto ldk = [&](int qi) SOL_INLINE {
+                return *reinterpret_cast<const KT*>(smem + kadr[qi >> 1] + KOFF + (qi & 1) * KT1);
             };
-            auto ldv = [&](int pi) {
+            auto ldv = [&](int pi) SOL_INLINE {
                 return *reinterpret_cast<const f16x8*>(smem + vadr[pi >> 2] + VOFF + (pi & 3) * VMT);
             };
-            bf16x8 kop[4];
+            KT kop[4];
             f16x8 vop[4];
             int nk = 0, nv = 0;   // operands loaded so far (ring of 4)
-            auto prefetch = [&](int sl) {
+            auto prefetch = [&](int sl) SOL_INLINE {
                 if (sl >= 32) return;
                 if (kind(sl) == 0) kop[(nk++) & 3] = ldk(index(sl));
                 else vop[(nv++) & 3] = ldv(index(sl));
@@ -967,9 +999,9 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
                 prefetch(sl + 2);
                 const int id = index(sl);
                 if (kind(sl) == 0) {
-                    const bf16x8 av = kop[(ck++) & 3];
-                    if (id & 1) n1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[id >> 1], n1, 0, 0, 0);
-                    else n0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qf[id >> 1], n0, 0, 0, 0);
+                    const KT av = kop[(ck++) & 3];
+                    if (id & 1) n1 = mfma_qk(av, qop[id >> 1], n1);
+                    else n0 = mfma_qk(av, qop[id >> 1], n0);
                 } else {
                     const f16x8 av = vop[(cv++) & 3];
                     o[id & 3] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, pb[id >> 2], o[id & 3], 0, 0, 0);
@@ -977,13 +1009,14 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
                 if (sl < 4) exp_pair(0, sl);
                 else if (sl < 28 && !((sl - 4) & 1)) exp_pair(((sl - 4) >> 3) + 1, ((sl - 4) & 7) >> 1);
             }
+            scores_done(t + 1, n0, n1);
             mx = tile_max(n0, n1);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             s0 = n0;
             s1 = n1;
         };
-        auto step = [&](auto par_tag, int t) {
+        auto step = [&](auto par_tag, int t) SOL_INLINE {
             if constexpr (D == 128) step_slots(par_tag, t);
             else step_generic(par_tag, t);
         };
@@ -996,12 +1029,32 @@ __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(2, 2))) 
             step(S0{}, t);
             ++t;
         }
-        // last tile (t == T-1): the only one that can be the ragged last key block
-        mask_tail(ecode(T - 1), s0, s1);
+        // last tile (t == T-1)
+        if constexpr (!APX) mask_tail(code(T - 1), s0, s1);
         f16x8 pb[4];
         softmax(s0, s1, pb);
         if ((T - 1) & 1) pv(S1{}, pb);
         else pv(S0{}, pb);
+    };
+
+    if (MODE == kSparse && napx > 0) {
+        f16x8 qh[NKS];
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks) {
+            const bf16x8 qv = qrow < a.N ? *reinterpret_cast<const bf16x8*>(qrow_p + 16 * ks) : bf16x8{};
+#pragma unroll
+            for (int e = 0; e < 8; ++e) qh[ks][e] = (_Float16)(float)qv[e];
+        }
+        pipeline(APX_T{}, qh, napx, [&](int t) SOL_INLINE { return list[t] & ~kApxFlag; });
+        __syncthreads();   // the stages are refilled below while the last V tile may still be read
+    }
+    const int T = ntiles - napx;
+    if (T > 0) {
+        bf16x8 qf[NKS];
+#pragma unroll
+        for (int ks = 0; ks < NKS; ++ks)
+            qf[ks] = qrow < a.N ? *reinterpret_cast<const bf16x8*>(qrow_p + 16 * ks) : bf16x8{};
+        pipeline(EXACT_T{}, qf, T, [&](int t) SOL_INLINE { return tile_code(napx + t); });
     }
 
     // ---- epilogue: O = O^T / l, bf16
