@@ -116,8 +116,9 @@ __global__ __launch_bounds__(256) void pool_mean_kernel(const T* __restrict__ x,
 
 // ---------------------------------------------------------------------------
 // K/V preparation for the bf16 forward.  grid (NJ, BH), 256 threads, one key block each.
-//   vt     [BH][D][Npad] f16: V^T with swap23 key order inside each 16-key segment; rows
-//          past N are zero.
+//   vt     [BH][NK][D][64] f16: V^T tile by tile (each key block's transposed values are
+//          one contiguous 16 KB run at d = 128), swap23 key order inside each 16-key
+//          segment; rows past N are zero.
 //   routing modes additionally:
 //   kbar   [BH][NK][D] f32 means (routing proxies and moments)
 //   kbarh  [BH][NC*64][D] f16 means of routable blocks (A operand of correction tiles);
@@ -130,7 +131,7 @@ template <int D>
 __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
                                                       float* __restrict__ kbar, _Float16* __restrict__ kbarh,
                                                       _Float16* __restrict__ vbart, _Float16* __restrict__ vt,
-                                                      int N, int NK, int NKr, int NC, int Npad, int routing) {
+                                                      int N, int NK, int NKr, int NC, int routing) {
     constexpr int CPR = D / 8;          // 16-byte chunks per row
     constexpr int GROUPS = 256 / CPR;   // row groups
     constexpr int VS = D + 2;           // f16 row stride of the staged V tile (odd word count)
@@ -149,22 +150,31 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict
     const int row0 = j * kBlockK;
     const int n = min(kBlockK, N - row0);
     const float inv = 1.0f / (float)n;
+    constexpr int RPT = kBlockK / GROUPS;   // rows per thread (4 or 2)
 
+    // All loads of the block are issued up front: the thread's rows of V and, in routing
+    // modes, of K (rows past N read as zero).
+    u32x4 vraw[RPT], kraw[RPT];
+    {
+        const uint16_t* vb = v + ((size_t)bh * N + row0) * D + cc * 8;
+        const uint16_t* kb = k + ((size_t)bh * N + row0) * D + cc * 8;
+#pragma unroll
+        for (int u = 0; u < RPT; ++u) {
+            const int r = g + u * GROUPS;
+            vraw[u] = r < n ? *reinterpret_cast<const u32x4*>(vb + (size_t)r * D) : u32x4{0u, 0u, 0u, 0u};
+            kraw[u] = (routing && r < n) ? *reinterpret_cast<const u32x4*>(kb + (size_t)r * D) : u32x4{0u, 0u, 0u, 0u};
+        }
+    }
     // ---- V: stage as f16 (exact for bf16 values inside the f16 range) and sum columns
     {
-        const uint16_t* base = v + ((size_t)bh * N + row0) * D + cc * 8;
         float acc[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-        for (int r = g; r < kBlockK; r += GROUPS) {
-            float f[8];
-            if (r < n) {
-                u32x4 c = *reinterpret_cast<const u32x4*>(base + (size_t)r * D);
-                Elem<uint16_t>::unpack(c, f);
-            } else {
 #pragma unroll
-                for (int e = 0; e < 8; ++e) f[e] = 0.f;
-            }
+        for (int u = 0; u < RPT; ++u) {
+            const int r = g + u * GROUPS;
+            float f[8];
+            Elem<uint16_t>::unpack(vraw[u], f);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 acc[e] += f[e];
@@ -182,7 +192,7 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict
         constexpr int TPR = 256 / D;             // threads per d row (2 or 4)
         constexpr int RUN = kBlockK / TPR;       // positions per thread (32 or 16)
         const int drow = t / TPR, p0 = (t % TPR) * RUN;
-        _Float16* dst = vt + ((size_t)bh * D + drow) * Npad + row0 + p0;
+        _Float16* dst = vt + (((size_t)bh * NK + j) * D + drow) * kBlockK + p0;
 #pragma unroll
         for (int u = 0; u < RUN; u += 8) {
             f16x8 pk;
@@ -202,14 +212,13 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict
     __syncthreads();
     // ---- K: column means
     {
-        const uint16_t* base = k + ((size_t)bh * N + row0) * D + cc * 8;
         float acc[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-        for (int r = g; r < n; r += GROUPS) {
-            u32x4 c = *reinterpret_cast<const u32x4*>(base + (size_t)r * D);
+#pragma unroll
+        for (int u = 0; u < RPT; ++u) {
             float f[8];
-            Elem<uint16_t>::unpack(c, f);
+            Elem<uint16_t>::unpack(kraw[u], f);
 #pragma unroll
             for (int e = 0; e < 8; ++e) acc[e] += f[e];
         }
@@ -232,10 +241,10 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict
 // kernels.  moments_partial_kernel: grid (kMomSplit, BH), 256 threads; split s accumulates,
 // in f64, S1 = sum_j x_j and S2 = sum_j x_j^T x_j over its share of the key blocks, with
 // x_j = Kbar_j - Kbar_0 (a shift that keeps the second moment well conditioned).
-// moments_final_kernel: grid (BH), sums the splits and writes mu_K = Kbar_0 + S1/n and
-// C_K = S2/n - (S1/n)^T (S1/n) in f32.
+// moments_final_kernel: grid (D*D/256, BH), sums the splits and writes mu_K = Kbar_0 + S1/n
+// and C_K = S2/n - (S1/n)^T (S1/n) in f32, 256 entries of C_K per workgroup.
 // ---------------------------------------------------------------------------
-constexpr int kMomSplit = 8;
+constexpr int kMomSplit = 16;
 
 // Device lambdas of the attention kernel are always inlined: a call would move the register
 // tile state through memory.
@@ -293,17 +302,18 @@ __global__ __launch_bounds__(256) void moments_final_kernel(const float* __restr
                                                             float* __restrict__ muk, float* __restrict__ cov, int NK,
                                                             int NKr) {
     __shared__ double m[D];
-    const int bh = blockIdx.x, t = threadIdx.x;
+    const int chunk = blockIdx.x, bh = blockIdx.y, t = threadIdx.x;
     const double* pp = part + (size_t)bh * kMomSplit * (D * D + D);
     const double inv = 1.0 / (double)NKr;
-    if (t < D) {
+    for (int c = t; c < D; c += 256) {
         double s = 0.0;
-        for (int sp = 0; sp < kMomSplit; ++sp) s += pp[(size_t)sp * (D * D + D) + D * D + t];
-        m[t] = s * inv;
-        muk[(size_t)bh * D + t] = (float)((double)kbar[(size_t)bh * NK * D + t] + m[t]);
+        for (int sp = 0; sp < kMomSplit; ++sp) s += pp[(size_t)sp * (D * D + D) + D * D + c];
+        m[c] = s * inv;
+        if (chunk == 0) muk[(size_t)bh * D + c] = (float)((double)kbar[(size_t)bh * NK * D + c] + m[c]);
     }
     __syncthreads();
-    for (int e = t; e < D * D; e += 256) {
+    const int e = chunk * 256 + t;
+    if (e < D * D) {
         double s = 0.0;
         for (int sp = 0; sp < kMomSplit; ++sp) s += pp[(size_t)sp * (D * D + D) + e];
         cov[(size_t)bh * D * D + e] = (float)(s * inv - m[e / D] * m[e % D]);
@@ -312,8 +322,11 @@ __global__ __launch_bounds__(256) void moments_final_kernel(const float* __restr
 
 // ---------------------------------------------------------------------------
 // Thresholds (Eq. threshold_routing with Eq. threshold_stats_exact).  grid (ceil(NQ/16), BH),
-// 256 threads; C_K staged in LDS.  256/D query blocks are processed at a time, D threads
-// each: thread r forms (C_K Qbar_i^T)_r, then sums over r give Qbar_i C_K Qbar_i^T.
+// 256 threads in 256/D groups of D.  Thread (g, r) holds column r of C_K (= row r, C_K is
+// symmetric) in registers and, for the group's query blocks i, forms y_r = (C_K Qbar_i^T)_r
+// from the staged Qbar rows (broadcast LDS reads); the D products Qbar_ir y_r and
+// Qbar_ir mu_r are summed per wave, and the wave partials per query block give
+// Qbar_i C_K Qbar_i^T and Qbar_i mu_K^T.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void tau_kernel(const float* __restrict__ qbar, const float* __restrict__ muk,
@@ -321,63 +334,67 @@ __global__ __launch_bounds__(256) void tau_kernel(const float* __restrict__ qbar
                                                   float* __restrict__ mu_out, float* __restrict__ sigma_out,
                                                   int NQ, float beta, float scale) {
     constexpr int QPB = 16;
-    constexpr int PAR = 256 / D;
-    extern __shared__ float smem_tau[];
-    float* C = smem_tau;              // D*D
-    float* qs = C + D * D;            // QPB*D
-    float* mk = qs + QPB * D;         // D
-    float* red = mk + D;              // 2 * 4 (partials per wave)
+    constexpr int PAR = 256 / D;      // groups
+    constexpr int WPG = D / 64;       // waves per group
+    __shared__ __attribute__((aligned(16))) float qs[QPB * D];
+    __shared__ float red[QPB][WPG][2];
     const int bh = blockIdx.y, i0 = blockIdx.x * QPB, t = threadIdx.x;
     const int nq = min(QPB, NQ - i0);
-    for (int e = t; e < D * D; e += 256) C[e] = cov[(size_t)bh * D * D + e];
+    const int g = t / D, r = t % D, wv = r / 64, lane = t & 63;
+    float ccol[D];
+#pragma unroll
+    for (int c = 0; c < D; ++c) ccol[c] = cov[((size_t)bh * D + c) * D + r];
+    const float mkr = muk[(size_t)bh * D + r];
     for (int e = t; e < nq * D; e += 256) qs[e] = qbar[((size_t)bh * NQ + i0) * D + e];
-    for (int e = t; e < D; e += 256) mk[e] = muk[(size_t)bh * D + e];
     __syncthreads();
-    const int which = t / D, r = t % D, lane = t & 63, wave = t >> 6;
-    for (int b = 0; b < QPB; b += PAR) {
-        const int qi = b + which;
-        float w = 0.f, m = 0.f;
-        if (qi < nq) {
-            float y = 0.f;
-            for (int c = 0; c < D; ++c) y += C[c * D + r] * qs[qi * D + c];  // C_K is symmetric
-            w = qs[qi * D + r] * y;
-            m = qs[qi * D + r] * mk[r];
+    for (int qq = g; qq < nq; qq += PAR) {
+        const float* qrow = qs + qq * D;
+        float y0 = 0.f, y1 = 0.f;
+#pragma unroll
+        for (int c = 0; c < D; c += 4) {
+            const f32x4 qv = *reinterpret_cast<const f32x4*>(qrow + c);
+            y0 = fmaf(ccol[c], qv[0], y0);
+            y1 = fmaf(ccol[c + 1], qv[1], y1);
+            y0 = fmaf(ccol[c + 2], qv[2], y0);
+            y1 = fmaf(ccol[c + 3], qv[3], y1);
         }
+        float w = qrow[r] * (y0 + y1);
+        float m = qrow[r] * mkr;
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) {
             w += __shfl_xor(w, off);
             m += __shfl_xor(m, off);
         }
         if (lane == 0) {
-            red[wave * 2] = w;
-            red[wave * 2 + 1] = m;
+            red[qq][wv][0] = w;
+            red[qq][wv][1] = m;
         }
-        __syncthreads();
-        if (r == 0 && qi < nq) {
-            constexpr int WPG = D / 64;  // waves per query block
-            float ws = 0.f, ms = 0.f;
-            for (int u = 0; u < WPG; ++u) {
-                ws += red[(wave + u) * 2];
-                ms += red[(wave + u) * 2 + 1];
-            }
-            const float mu = scale * ms;
-            const float sigma = scale * sqrtf(fmaxf(ws, 0.f));
-            float th;
-            if (beta == kNegInf) th = kNegInf;
-            else if (beta == -kNegInf) th = -kNegInf;
-            else th = mu + beta * sigma;
-            const size_t o = (size_t)bh * NQ + i0 + qi;
-            tau[o] = th;
-            if (mu_out) mu_out[o] = mu;
-            if (sigma_out) sigma_out[o] = sigma;
+    }
+    __syncthreads();
+    if (t < nq) {
+        float ws = 0.f, ms = 0.f;
+#pragma unroll
+        for (int u = 0; u < WPG; ++u) {
+            ws += red[t][u][0];
+            ms += red[t][u][1];
         }
-        __syncthreads();
+        const float mu = scale * ms;
+        const float sigma = scale * sqrtf(fmaxf(ws, 0.f));
+        float th;
+        if (beta == kNegInf) th = kNegInf;
+        else if (beta == -kNegInf) th = -kNegInf;
+        else th = mu + beta * sigma;
+        const size_t o = (size_t)bh * NQ + i0 + t;
+        tau[o] = th;
+        if (mu_out) mu_out[o] = mu;
+        if (sigma_out) sigma_out[o] = sigma;
     }
 }
 
 // ---------------------------------------------------------------------------
-// Routing prologue shared by both attention kernels: selection bits of every routable key
-// block for query block qi into selw (LDS), then the tile list:
+// Routing prologue shared by both attention kernels: the f32 proxy of every routable key
+// block (pooled query . pooled key, scaled) against the row threshold (strict >) gives its
+// selection bit for query block qi in selw (LDS); then the tile list:
 //   [correction tiles: every chunk c of 64 routable blocks with an unselected valid block,
 //    sparse mode only, encoded kApxFlag | c] [selected routable blocks, increasing j]
 //   [forced blocks].
@@ -412,48 +429,34 @@ __device__ int block_scan_incl(int v, int* scratch, int* total) {
 
 template <int D, int NT, int MODE>
 __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __restrict__ kbar_h, float tau_i,
-                              float scale, int NKr, int NK, int MW, int NC, float* qb_s, uint32_t* selw,
-                              char* stages, int* list, int* scan_scratch, int* napx, int* nsel) {
-    constexpr int NW = NT / 64;
+                              float scale, int NKr, int NK, int MW, int NC, uint32_t* selw, int* list,
+                              int* scan_scratch, int* napx, int* nsel) {
     constexpr int CPR = D / 4;              // 16-byte chunks per f32 pooled-key row
-    constexpr int WL = CPR / NW;            // wave loads per wave for one chunk of 64 rows
     constexpr int TPK = NT / kChunk;        // threads per pooled key (1, 2 or 4)
+    constexpr int CPT = CPR / TPK;          // 16-byte chunks of a row per thread
     constexpr int KPWV = 64 / TPK;          // pooled keys per wave (64, 32 or 16)
     static_assert(NT % kChunk == 0 && TPK <= 4, "routing expects 64..256 threads");
-    constexpr int STAGE = kChunk * D * 4;   // one chunk of f32 pooled keys == one tile stage
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    for (int c = tid; c < D; c += NT) qb_s[c] = qbar_i[c];
-    for (int w = tid; w < MW; w += NT) selw[w] = 0u;
-    // Chunk c of pooled keys -> stage (c & 1); row r's 16-byte chunk cc sits at position
-    // r*CPR + (cc ^ (4r mod CPR)) so that the 4-lane groups below read distinct banks.
-    auto issue = [&](int c, int buf) {
-        char* st = stages + buf * STAGE;
-#pragma unroll
-        for (int u = 0; u < WL; ++u) {
-            const int w0 = (wave * WL + u) * 64;
-            const int r = (w0 + lane) / CPR;
-            const int cc = (lane % CPR) ^ ((4 * r) & (CPR - 1));
-            const int row = min(c * kChunk + r, NKr - 1);
-            __builtin_amdgcn_global_load_lds(kbar_h + (size_t)row * D + cc * 4,
-                                             (__attribute__((address_space(3))) void*)(st + w0 * 16), 16, 0, 0);
-        }
-    };
-    issue(0, 0);
     const int jl = tid / TPK, seg = tid % TPK;
-    for (int c = 0; c < NC; ++c) {
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        if (c + 1 < NC) issue(c + 1, (c + 1) & 1);
-        const char* st = stages + (c & 1) * STAGE;
+    // Each thread streams its share (chunks seg, seg+TPK, ...) of one pooled-key row per group
+    // of 64 keys straight from L2 into registers, up to three groups in flight; the pooled
+    // query stays in registers.  No LDS staging and no barrier until all proxies are decided.
+    f32x4 qv[CPT];
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) qv[i] = *reinterpret_cast<const f32x4*>(qbar_i + 4 * (seg + TPK * i));
+    auto load = [&](int c, f32x4 (&kv)[CPT]) SOL_INLINE {
+        const float* rp = kbar_h + (size_t)min(c * kChunk + jl, NKr - 1) * D;
+#pragma unroll
+        for (int i = 0; i < CPT; ++i) kv[i] = *reinterpret_cast<const f32x4*>(rp + 4 * (seg + TPK * i));
+    };
+    auto decide = [&](int c, const f32x4 (&kv)[CPT]) SOL_INLINE {
         float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
 #pragma unroll
-        for (int i = 0; i < CPR / TPK; ++i) {
-            const int cc = seg + TPK * i;
-            const f32x4 kv = *reinterpret_cast<const f32x4*>(st + 16 * (jl * CPR + (cc ^ ((4 * jl) & (CPR - 1)))));
-            a0 = fmaf(qb_s[4 * cc + 0], kv[0], a0);
-            a1 = fmaf(qb_s[4 * cc + 1], kv[1], a1);
-            a2 = fmaf(qb_s[4 * cc + 2], kv[2], a2);
-            a3 = fmaf(qb_s[4 * cc + 3], kv[3], a3);
+        for (int i = 0; i < CPT; ++i) {
+            a0 = fmaf(qv[i][0], kv[i][0], a0);
+            a1 = fmaf(qv[i][1], kv[i][1], a1);
+            a2 = fmaf(qv[i][2], kv[i][2], a2);
+            a3 = fmaf(qv[i][3], kv[i][3], a3);
         }
         float dot = (a0 + a1) + (a2 + a3);
 #pragma unroll
@@ -468,11 +471,26 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
             const int bit0 = c * kChunk + wave * KPWV;
             if constexpr (KPWV == 64) {
                 selw[bit0 >> 5] = (uint32_t)bits;
-                selw[(bit0 >> 5) + 1] = (uint32_t)(bits >> 32);
+                if ((bit0 >> 5) + 1 < MW) selw[(bit0 >> 5) + 1] = (uint32_t)(bits >> 32);
             } else if constexpr (KPWV == 32) {
-                selw[bit0 >> 5] = (uint32_t)bits;
+                if ((bit0 >> 5) < MW) selw[bit0 >> 5] = (uint32_t)bits;
             } else {
-                reinterpret_cast<uint16_t*>(selw)[bit0 >> 4] = (uint16_t)bits;
+                if ((bit0 >> 5) < MW) reinterpret_cast<uint16_t*>(selw)[bit0 >> 4] = (uint16_t)bits;
+            }
+        }
+    };
+    // ring of NB groups in flight (fewer when a thread's share of a row is large)
+    constexpr int NB = CPT <= 8 ? 3 : (CPT <= 16 ? 2 : 1);
+    f32x4 kb[NB][CPT];
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+        if (b < NC) load(b, kb[b]);
+    for (int c = 0; c < NC; c += NB) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            if (c + b < NC) {
+                decide(c + b, kb[b]);
+                if (c + b + NB < NC) load(c + b + NB, kb[b]);
             }
         }
     }
@@ -534,7 +552,7 @@ struct AttnArgs {
     uint16_t* out;
     uint32_t* blkcount;
     uint32_t* mask_out;
-    int BH, N, NQ, NK, NKr, Npad, NC, MW, per_x;
+    int BH, N, NQ, NK, NKr, NC, MW, per_x;
     float scale, c_log2;
     float bias_full, bias_last;   // log2(n_j)/c_log2 for full blocks and for the last block
 };
@@ -628,9 +646,8 @@ void routed_attn_kernel(AttnArgs a) {
 
     char* rest = smem + 2 * L::STAGE;
     int* scan_scratch = reinterpret_cast<int*>(rest);
-    float* qb_s = reinterpret_cast<float*>(rest + 64);
-    uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64 + 4 * D);
-    int* list = reinterpret_cast<int*>(rest + 64 + 4 * D + 4 * ((a.MW + 3) & ~3));
+    uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64);
+    int* list = reinterpret_cast<int*>(rest + 64 + 4 * ((a.MW + 3) & ~3));
 
     int ntiles, nsel, napx = 0;
     if (MODE == kDense) {
@@ -638,8 +655,8 @@ void routed_attn_kernel(AttnArgs a) {
         nsel = a.NKr;
     } else {
         ntiles = route_and_list<D, NT, MODE>(a.qbar + ((size_t)bh * a.NQ + qi) * D, a.kbar + (size_t)bh * a.NK * D,
-                                             a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, qb_s,
-                                             selw, smem, list, scan_scratch, &napx, &nsel);
+                                             a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, selw,
+                                             list, scan_scratch, &napx, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
@@ -669,7 +686,7 @@ void routed_attn_kernel(AttnArgs a) {
     auto vofs_calc = [&](int u) SOL_INLINE -> uint32_t {
         int r, c;
         L::vsrc((wave * VPW + u) * 64 + lane, r, c);
-        return (uint32_t)(r * a.Npad + c * 8) * 2u;
+        return (uint32_t)(r * kBlockK + c * 8) * 2u;
     };
     uint32_t koff[kKeepOff ? KPW : 1], voff[kKeepOff ? VPW : 1];
     if constexpr (kKeepOff) {
@@ -727,7 +744,7 @@ void routed_attn_kernel(AttnArgs a) {
     // ... and its transposed values into stage `buf`'s V region.
     auto issue_exact_v = [&](int j, int buf) SOL_INLINE {
         char* stage = smem + buf * L::STAGE;
-        const char* vp = reinterpret_cast<const char*>(a.vt + (size_t)bh * D * a.Npad + (size_t)j * kBlockK);
+        const char* vp = reinterpret_cast<const char*>(a.vt + ((size_t)bh * a.NK + j) * D * kBlockK);
 #pragma unroll
         for (int u = 0; u < VPW; ++u)
             lds_copy16(vp + vofs(u), (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024));
@@ -1106,9 +1123,8 @@ __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
     float* qt = vs + kBlockK * D;                          // [D][BQ]
     char* rest = reinterpret_cast<char*>(qt + D * BQ);
     int* scan_scratch = reinterpret_cast<int*>(rest);
-    float* qb_s = reinterpret_cast<float*>(rest + 64);
-    uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64 + 4 * D);
-    int* list = reinterpret_cast<int*>(rest + 64 + 4 * D + 4 * ((a.MW + 3) & ~3));
+    uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64);
+    int* list = reinterpret_cast<int*>(rest + 64 + 4 * ((a.MW + 3) & ~3));
 
     const int bh = blockIdx.y, qi = blockIdx.x, tid = threadIdx.x;
     int ntiles, nsel, napx = 0;
@@ -1117,8 +1133,8 @@ __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
         nsel = a.NKr;
     } else {
         ntiles = route_and_list<D, NT, MODE>(a.qbar + ((size_t)bh * a.NQ + qi) * D, a.kbar + (size_t)bh * a.NK * D,
-                                             a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, qb_s,
-                                             selw, smem, list, scan_scratch, &napx, &nsel);
+                                             a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, selw,
+                                             list, scan_scratch, &napx, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
@@ -1272,7 +1288,7 @@ Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype
 }
 
 size_t attn_lds_bytes(const Shape& s) {
-    const size_t rest = 64 + 4 * (size_t)s.d + 4 * (size_t)((s.MW + 3) & ~3) + 4 * (size_t)(s.NK + s.NC);
+    const size_t rest = 64 + 4 * (size_t)((s.MW + 3) & ~3) + 4 * (size_t)(s.NK + s.NC);
     if (s.dtype == kBF16) {
         const size_t stage = (size_t)kBlockK * s.d * 2 * 2;
         return 2 * stage + rest;
@@ -1327,10 +1343,10 @@ hipError_t launch_moments(const float* kbar, float* muk, float* cov, double* scr
                           hipStream_t st) {
     if (d == 128) {
         moments_partial_kernel<128><<<dim3(kMomSplit, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr);
-        moments_final_kernel<128><<<dim3(BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr);
+        moments_final_kernel<128><<<dim3(128 * 128 / 256, BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr);
     } else {
         moments_partial_kernel<64><<<dim3(kMomSplit, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr);
-        moments_final_kernel<64><<<dim3(BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr);
+        moments_final_kernel<64><<<dim3(64 * 64 / 256, BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr);
     }
     return hipGetLastError();
 }
@@ -1338,17 +1354,9 @@ hipError_t launch_moments(const float* kbar, float* muk, float* cov, double* scr
 hipError_t launch_tau(const float* qbar, const float* muk, const float* cov, float* tau, float* mu, float* sigma,
                       int BH, int NQ, int d, float beta, hipStream_t st) {
     const float scale = 1.0f / sqrtf((float)d);
-    const size_t lds = ((size_t)d * d + 16 * d + d + 8) * 4;
     const dim3 grid((NQ + 15) / 16, BH);
-    if (d == 128) {
-        hipError_t e = allow_lds(tau_kernel<128>, lds);
-        if (e != hipSuccess) return e;
-        tau_kernel<128><<<grid, dim3(256), lds, st>>>(qbar, muk, cov, tau, mu, sigma, NQ, beta, scale);
-    } else {
-        hipError_t e = allow_lds(tau_kernel<64>, lds);
-        if (e != hipSuccess) return e;
-        tau_kernel<64><<<grid, dim3(256), lds, st>>>(qbar, muk, cov, tau, mu, sigma, NQ, beta, scale);
-    }
+    if (d == 128) tau_kernel<128><<<grid, dim3(256), 0, st>>>(qbar, muk, cov, tau, mu, sigma, NQ, beta, scale);
+    else tau_kernel<64><<<grid, dim3(256), 0, st>>>(qbar, muk, cov, tau, mu, sigma, NQ, beta, scale);
     return hipGetLastError();
 }
 
@@ -1369,10 +1377,10 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         const uint16_t* vv = static_cast<const uint16_t*>(v);
         if (d == 128)
             prep_kv_kernel<128><<<dim3(nj, s.BH), dim3(256), 0, st>>>(kk, vv, ws.kbar, ws.kbarh, ws.vbart, ws.vt, s.N,
-                                                                      s.NK, s.NKr, s.NC, s.Npad, routing ? 1 : 0);
+                                                                      s.NK, s.NKr, s.NC, routing ? 1 : 0);
         else
             prep_kv_kernel<64><<<dim3(nj, s.BH), dim3(256), 0, st>>>(kk, vv, ws.kbar, ws.kbarh, ws.vbart, ws.vt, s.N,
-                                                                     s.NK, s.NKr, s.NC, s.Npad, routing ? 1 : 0);
+                                                                     s.NK, s.NKr, s.NC, routing ? 1 : 0);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (routing) {
             if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, ws.mom, s.BH, s.NK, s.NKr, d, st)) != hipSuccess) return e;
@@ -1391,7 +1399,7 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         a.out = static_cast<uint16_t*>(out);
         a.blkcount = ws.blkcount;
         a.mask_out = mask_out;
-        a.BH = s.BH; a.N = s.N; a.NQ = s.NQ; a.NK = s.NK; a.NKr = s.NKr; a.Npad = s.Npad; a.NC = s.NC; a.MW = s.MW;
+        a.BH = s.BH; a.N = s.N; a.NQ = s.NQ; a.NK = s.NK; a.NKr = s.NKr; a.NC = s.NC; a.MW = s.MW;
         a.per_x = (s.NQ + 7) / 8;
         a.scale = scale;
         a.c_log2 = scale * kLog2e;
