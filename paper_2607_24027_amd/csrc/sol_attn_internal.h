@@ -31,7 +31,7 @@ struct Workspace {
     float* kbar = nullptr;       // [BH][NK][d]
     float* vbar = nullptr;       // [BH][NK][d]            (f32 path)
     _Float16* kbarh = nullptr;   // [BH][NC*64][d] f16      (bf16 routing modes)
-    _Float16* vbart = nullptr;   // [BH][NC][d][64] f16     (bf16 sparse)
+    _Float16* vbarh = nullptr;   // [BH][NC*64][d] f16      (bf16 sparse)
     _Float16* vt = nullptr;      // [BH][NK][d][64] f16     (bf16)
     float* muk = nullptr;        // [BH][d]
     float* cov = nullptr;        // [BH][d][d]

@@ -121,16 +121,15 @@ __global__ __launch_bounds__(256) void pool_mean_kernel(const T* __restrict__ x,
 //          segment; rows past N are zero.
 //   routing modes additionally:
 //   kbar   [BH][NK][D] f32 means (routing proxies and moments)
-//   kbarh  [BH][NC*64][D] f16 means of routable blocks (A operand of correction tiles);
+//   kbarh  [BH][NC*64][D] f16 key means of routable blocks (gathered into correction tiles);
 //          zero for forced and padding rows
-//   vbart  [BH][NC][D][64] f16 value means in correction layout (slot swap23(j%64));
-//          zero for forced and padding slots
+//   vbarh  [BH][NC*64][D] f16 value means, same rows
 // Blocks j >= NK exist only to zero the padding rows of the last correction tile.
 // ---------------------------------------------------------------------------
 template <int D>
 __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
                                                       float* __restrict__ kbar, _Float16* __restrict__ kbarh,
-                                                      _Float16* __restrict__ vbart, _Float16* __restrict__ vt,
+                                                      _Float16* __restrict__ vbarh, _Float16* __restrict__ vt,
                                                       int N, int NK, int NKr, int NC, int routing) {
     constexpr int CPR = D / 8;          // 16-byte chunks per row
     constexpr int GROUPS = 256 / CPR;   // row groups
@@ -143,7 +142,7 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict
     if (j >= NK) {  // padding rows of the last correction tile
         for (int c = t; c < D; c += 256) {
             kbarh[((size_t)bh * NC * kChunk + j) * D + c] = (_Float16)0.f;
-            vbart[(((size_t)bh * NC + j / kChunk) * D + c) * kChunk + swap23(j % kChunk)] = (_Float16)0.f;
+            vbarh[((size_t)bh * NC * kChunk + j) * D + c] = (_Float16)0.f;
         }
         return;
     }
@@ -206,8 +205,7 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict
         float s = 0.f;
         for (int gg = 0; gg < GROUPS; ++gg) s += red[gg * D + t];
         const bool routable = j < NKr;
-        vbart[(((size_t)bh * NC + j / kChunk) * D + t) * kChunk + swap23(j % kChunk)] =
-            routable ? (_Float16)(s * inv) : (_Float16)0.f;
+        vbarh[((size_t)bh * NC * kChunk + j) * D + t] = routable ? (_Float16)(s * inv) : (_Float16)0.f;
     }
     __syncthreads();
     // ---- K: column means
@@ -394,15 +392,15 @@ __global__ __launch_bounds__(256) void tau_kernel(const float* __restrict__ qbar
 // ---------------------------------------------------------------------------
 // Routing prologue shared by both attention kernels: the f32 proxy of every routable key
 // block (pooled query . pooled key, scaled) against the row threshold (strict >) gives its
-// selection bit for query block qi in selw (LDS); then the tile list:
-//   [correction tiles: every chunk c of 64 routable blocks with an unselected valid block,
-//    sparse mode only, encoded kApxFlag | c] [selected routable blocks, increasing j]
-//   [forced blocks].
-// The online softmax is order independent, so grouping the correction tiles first changes
-// only the floating-point summation order.  Returns the list length; *napx receives the
-// number of correction tiles and *nsel the number of selected routable blocks.
+// selection bit for query block qi in selw (LDS); then two lists (LDS, 16-bit):
+//   list[0, NKr)   the unselected routable blocks in increasing j (sparse mode): the slots
+//                  of the correction tiles, 64 per tile, the last tile padded;
+//   list[NKr, ...) the exact tiles: selected routable blocks in increasing j, then the
+//                  forced blocks.
+// The online softmax is order independent, so running the correction tiles first changes
+// only the floating-point summation order.  Returns the number of exact tiles; *nuns
+// receives the number of unselected routable blocks and *nsel of selected ones.
 // ---------------------------------------------------------------------------
-constexpr int kApxFlag = 1 << 30;
 
 template <int NT>
 __device__ int block_scan_incl(int v, int* scratch, int* total) {
@@ -429,8 +427,8 @@ __device__ int block_scan_incl(int v, int* scratch, int* total) {
 
 template <int D, int NT, int MODE>
 __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __restrict__ kbar_h, float tau_i,
-                              float scale, int NKr, int NK, int MW, int NC, uint32_t* selw, int* list,
-                              int* scan_scratch, int* napx, int* nsel) {
+                              float scale, int NKr, int NK, int MW, int NC, uint32_t* selw, uint16_t* list,
+                              int* scan_scratch, int* nuns, int* nsel) {
     constexpr int CPR = D / 4;              // 16-byte chunks per f32 pooled-key row
     constexpr int TPK = NT / kChunk;        // threads per pooled key (1, 2 or 4)
     constexpr int CPT = CPR / TPK;          // 16-byte chunks of a row per thread
@@ -500,17 +498,29 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
         const uint32_t hi = (2 * c + 1 < MW) ? selw[2 * c + 1] : 0u;
         return (uint64_t)lo | ((uint64_t)hi << 32);
     };
-    // pass 1: correction tiles
-    int n_apx = 0;
+    uint16_t* ulist = list;         // unselected routable blocks, increasing j (sparse mode)
+    uint16_t* elist = list + NKr;   // selected routable blocks, increasing j, then the forced ones
+    // pass 1: unselected routable blocks (the correction slots)
+    int n_uns = 0;
     if (MODE == kSparse) {
         for (int c0 = 0; c0 < NC; c0 += NT) {
             const int c = c0 + tid;
-            int apx = 0;
-            if (c < NC) apx = __popcll(chunk_bits(c)) < min(kChunk, NKr - c * kChunk) ? 1 : 0;
+            uint64_t ub = 0;
+            if (c < NC) {
+                const int nvalid = min(kChunk, NKr - c * kChunk);
+                const uint64_t valid = nvalid >= 64 ? ~0ull : ((1ull << nvalid) - 1ull);
+                ub = ~chunk_bits(c) & valid;
+            }
+            const int nu = __popcll(ub);
             int tot;
-            const int incl = block_scan_incl<NT>(apx, scan_scratch, &tot);
-            if (apx) list[n_apx + incl - 1] = kApxFlag | c;
-            n_apx += tot;
+            const int incl = block_scan_incl<NT>(nu, scan_scratch, &tot);
+            int pos = n_uns + incl - nu;
+            while (ub) {
+                const int b = __builtin_ctzll(ub);
+                ub &= ub - 1;
+                ulist[pos++] = (uint16_t)(c * kChunk + b);
+            }
+            n_uns += tot;
         }
     }
     // pass 2: selected blocks in increasing order
@@ -521,20 +531,19 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
         const int ns = __popcll(bits);
         int tot;
         const int incl = block_scan_incl<NT>(ns, scan_scratch, &tot);
-        int pos = n_apx + n_sel + incl - ns;
+        int pos = n_sel + incl - ns;
         while (bits) {
             const int b = __builtin_ctzll(bits);
             bits &= bits - 1;
-            list[pos++] = c * kChunk + b;
+            elist[pos++] = (uint16_t)(c * kChunk + b);
         }
         n_sel += tot;
     }
-    const int n_exact0 = n_apx + n_sel;
-    for (int j = NKr + tid; j < NK; j += NT) list[n_exact0 + (j - NKr)] = j;
+    for (int j = NKr + tid; j < NK; j += NT) elist[n_sel + (j - NKr)] = (uint16_t)j;
     __syncthreads();
-    *napx = n_apx;
+    *nuns = n_uns;
     *nsel = n_sel;
-    return n_exact0 + (NK - NKr);
+    return n_sel + (NK - NKr);
 }
 
 // ---------------------------------------------------------------------------
@@ -547,7 +556,7 @@ struct AttnArgs {
     const float* qbar;
     const float* kbar;
     const _Float16* kbarh;
-    const _Float16* vbart;
+    const _Float16* vbarh;
     const float* tau;
     uint16_t* out;
     uint32_t* blkcount;
@@ -599,9 +608,30 @@ struct TileLds {
         r = 2 * R + (C >> 3);
         c = C & 7;
     }
+    // Correction tiles keep their value means row-major in the V region: slot s at s * 2D
+    // bytes, chunk q of the row holding chunk q ^ rswz(s).  The correction PV reads it with
+    // transposed loads, 32 lanes covering 4 consecutive slots x 4 consecutive chunks; rswz
+    // puts those 16 chunks in distinct bank groups.
+    static constexpr int RCPR = D / 8;
+    __device__ static int rswz(int s) { return RCPR == 16 ? 4 * (s & 3) : 4 * ((s >> 1) & 1); }
+    __device__ static void rsrc(int p, int& s, int& c) {
+        s = p / RCPR;
+        c = (p % RCPR) ^ rswz(s);
+    }
 };
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) s16x4* lds_s16x4_ptr;
+
+// Transposed LDS read (ds_read_b64_tr_b16).  Within each group of 16 lanes, lane j supplies
+// the address of 4 consecutive 16-bit values R_j; lane i receives R_{4e + i/4}[i % 4] for
+// e = 0..3.  With lane j pointing at row j/4, columns 4*(j%4).., lane i gets column i of
+// 4 consecutive rows.
+__device__ __forceinline__ s16x4 lds_read_tr16(const char* p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr)(p));
+}
 
 // Direct global->LDS copy of 16 bytes per lane (LDS bytes [dst + 16*lane, +16)), written as
 // inline assembly so that the compiler's wait-count model does not track it: the exact-tile
@@ -647,20 +677,25 @@ void routed_attn_kernel(AttnArgs a) {
     char* rest = smem + 2 * L::STAGE;
     int* scan_scratch = reinterpret_cast<int*>(rest);
     uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64);
-    int* list = reinterpret_cast<int*>(rest + 64 + 4 * ((a.MW + 3) & ~3));
+    uint16_t* list = reinterpret_cast<uint16_t*>(rest + 64 + 4 * ((a.MW + 3) & ~3));
+    const uint16_t* ulist = list;            // correction slots (unselected routable blocks)
+    const uint16_t* elist = list + a.NKr;    // exact tiles
 
-    int ntiles, nsel, napx = 0;
+    int ntiles, nsel, nuns = 0;
     if (MODE == kDense) {
         ntiles = a.NK;
         nsel = a.NKr;
     } else {
         ntiles = route_and_list<D, NT, MODE>(a.qbar + ((size_t)bh * a.NQ + qi) * D, a.kbar + (size_t)bh * a.NK * D,
                                              a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, selw,
-                                             list, scan_scratch, &napx, &nsel);
+                                             list, scan_scratch, &nuns, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
     if (tid == 0) a.blkcount[(size_t)bh * a.NQ + qi] = (uint32_t)nsel;
+    const int napx = MODE == kSparse ? (nuns + kChunk - 1) / kChunk : 0;   // correction tiles
+    // slot of the ragged last key block among the correction slots (it can only be the last one)
+    const int last_slot = (nuns > 0 && a.NKr == a.NK && ulist[max(nuns - 1, 0)] == a.NK - 1) ? nuns - 1 : -1;
 
     const int qrow = qi * BQ + wave * 32 + r32;
     const uint16_t* qrow_p = a.q + ((size_t)bh * a.N + min(qrow, a.N - 1)) * D + 8 * hh;
@@ -670,7 +705,7 @@ void routed_attn_kernel(AttnArgs a) {
     for (int mt = 0; mt < NDT; ++mt) o[mt] = f32x16{};
     float m_run = kNegInf, l_run = 0.f;
 
-    auto tile_code = [&](int n) -> int { return MODE == kDense ? n : list[n]; };
+    auto tile_code = [&](int n) -> int { return MODE == kDense ? n : (int)elist[n]; };
     // Global->LDS copies.  Each lane moves one 16-byte chunk per instruction; the per-lane
     // byte offsets inside a tile are fixed, so they are computed once here and each tile only
     // adds wave-uniform base pointers.  Rows past the end of the sequence (ragged last block)
@@ -703,23 +738,43 @@ void routed_attn_kernel(AttnArgs a) {
         if constexpr (kKeepOff) return voff[u];
         else return vofs_calc(u);
     };
-    // Copies of a correction tile: the f16 pooled keys of chunk c into stage `buf`'s K region ...
+    // Copies of correction tile c: the f16 pooled keys of its 64 slots (gathered rows; padding
+    // slots past the unselected blocks copy row 0, their scores are masked) into stage `buf`'s
+    // K region, K layout ...
+    auto slot_row = [&](int c, int r) SOL_INLINE -> int {
+        const int u = c * kChunk + r;
+        const int j = ulist[min(u, nuns - 1)];   // nuns >= 1 whenever a correction tile exists
+        return u < nuns ? j : 0;
+    };
+    const char* kbh_base = reinterpret_cast<const char*>(a.kbarh + (size_t)bh * a.NC * kChunk * D);
+    const char* vbh_base = reinterpret_cast<const char*>(a.vbarh + (size_t)bh * a.NC * kChunk * D);
     auto issue_apx_k = [&](int c, int buf) SOL_INLINE {
         char* stage = smem + buf * L::STAGE;
-        const char* kp = reinterpret_cast<const char*>(a.kbarh + ((size_t)bh * a.NC * kChunk + (size_t)c * kChunk) * D);
 #pragma unroll
-        for (int u = 0; u < KPW; ++u) lds_copy16(kp + kofs(u), (lds_ptr_t)(stage + (wave * KPW + u) * 1024));
+        for (int u = 0; u < KPW; ++u) {
+            int r, cc;
+            if constexpr (L::KCPR == 16) {   // copy u covers rows 4(wave*KPW+u) .. +3, 16 lanes each
+                r = 4 * (wave * KPW + u) + (lane >> 4);
+                cc = (lane & 15) ^ (r & 15);
+            } else {
+                L::ksrc((wave * KPW + u) * 64 + lane, r, cc);
+            }
+            lds_copy16(kbh_base + ((size_t)slot_row(c, r) * D + cc * 8) * 2,
+                       (lds_ptr_t)(stage + (wave * KPW + u) * 1024));
+        }
     };
-    // ... and their transposed f16 value means into its V region ...
+    // ... and the f16 value means of the same rows into its V region, row-major (slot s at
+    // s * 2D bytes, 16-byte chunk q of a row holding chunk q ^ rswz(s)), read back transposed
+    // by the correction PV ...
     auto issue_apx_v = [&](int c, int buf) SOL_INLINE {
         char* stage = smem + buf * L::STAGE;
-        const char* vp = reinterpret_cast<const char*>(a.vbart + ((size_t)bh * a.NC + c) * D * kChunk);
+        constexpr int LPR = L::RCPR;                  // lanes per row of a copy
+        const int cc = (lane % LPR) ^ L::rswz(lane / LPR);   // rswz depends on the row mod 4
 #pragma unroll
         for (int u = 0; u < VPW; ++u) {
-            int r, cc;
-            L::vsrc((wave * VPW + u) * 64 + lane, r, cc);
-            const uint32_t off = (uint32_t)(r * kChunk + cc * 8) * 2u;
-            lds_copy16(vp + off, (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024));
+            const int r = (64 / LPR) * (wave * VPW + u) + lane / LPR;
+            lds_copy16(vbh_base + ((size_t)slot_row(c, r) * D + cc * 8) * 2,
+                       (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024));
         }
     };
     // ... and of an exact tile: key block j into stage `buf`'s K region ...
@@ -764,6 +819,27 @@ void routed_attn_kernel(AttnArgs a) {
     for (int kk = 0; kk < 4; ++kk) vadr[kk] = (uint32_t)L::KBYTES + 16u * (uint32_t)L::vpos(r32, 2 * kk + hh);
     constexpr int KT1 = 32 * L::KCPR * 16;   // byte offset of K rows 32..63
     constexpr int VMT = 32 * L::VCPR * 16;   // byte offset between V^T M-tiles
+    // Correction PV: the A operand (value means transposed: 32 values of d x 8 slots) of
+    // M-tile mt and k-step kk comes from two transposed reads, slots 16kk + 4hh + 0..3 and
+    // 16kk + 8 + 4hh + 0..3 (the slot order of the score registers); this lane reads row
+    // 4hh + (lane%16)/4 (+16kk, +8) at d = 32mt + 16*((lane/16)%2) + 4*(lane%4).  The row
+    // swizzle depends only on the row modulo 4, so kk and the second read add whole rows.
+    uint32_t vtr[NDT];
+    {
+        const int s0 = 4 * hh + ((lane & 15) >> 2);
+#pragma unroll
+        for (int mt = 0; mt < NDT; ++mt) {
+            const int cc = 4 * mt + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
+            vtr[mt] = (uint32_t)(L::KBYTES + s0 * 2 * D + 16 * (cc ^ L::rswz(s0)) + 8 * (lane & 1));
+        }
+    }
+    auto ldv_apx = [&](int kk, int mt, int soff) SOL_INLINE -> f16x8 {
+        const char* p = smem + vtr[mt] + soff + kk * 16 * 2 * D;
+        const s16x4 lo = lds_read_tr16(p);
+        const s16x4 hi = lds_read_tr16(p + 8 * 2 * D);
+        const s16x8 both = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        return __builtin_bit_cast(f16x8, both);
+    };
 
     // S^T = K Q^T over two 32-key M-tiles, operands double-buffered in registers.  Exact
     // tiles: bf16 keys x bf16 queries.  Correction tiles: f16 pooled keys x f16 queries, so the
@@ -806,22 +882,20 @@ void routed_attn_kernel(AttnArgs a) {
     // solattn_denominator) unless it is selected (exact tile) or past the routable keys.
     auto bias_apx = [&](int c, f32x16& s0, f32x16& s1) SOL_INLINE {
         // Element r of this lane's score registers holds slot 4*hh + off(r) (s0) or 32 + that
-        // (s1), off(r) = 8*(r/4) + r%4.  Per slot half, one word marks the slots that take the
-        // bias (valid and unselected); shifting it by 4*hh leaves compile-time bit positions.
-        const int nvalid = min(kChunk, a.NKr - c * kChunk);
-        const uint32_t vlo = nvalid >= 32 ? 0xffffffffu : (nvalid <= 0 ? 0u : ((1u << nvalid) - 1u));
-        const uint32_t vhi = nvalid >= 64 ? 0xffffffffu : (nvalid <= 32 ? 0u : ((1u << (nvalid - 32)) - 1u));
-        const uint32_t whi = 2 * c + 1 < a.MW ? selw[2 * c + 1] : 0u;
-        const uint32_t blo = (~selw[2 * c] & vlo) >> (4 * hh);
-        const uint32_t bhi = (~whi & vhi) >> (4 * hh);
-        const int last = a.NK - 1 - c * kChunk - 4 * hh;   // off() of the (possibly short) last block
+        // (s1), off(r) = 8*(r/4) + r%4.  Slots below nv are unselected routable blocks and take
+        // the multiplicity bias (log2 n_j); the rest of the last tile is padding.
+        int nv = nuns - c * kChunk - 4 * hh;      // off() bound of the valid slots
+        int last = last_slot - c * kChunk - 4 * hh;
+        // opaque here, so that the 32 biases are formed where they are added and not hoisted
+        // into the MFMA slots of the iteration, where they would hold 32 registers
+        asm volatile("" : "+v"(nv), "+v"(last));
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int off = 8 * (r >> 2) + (r & 3);
             const float b0 = (off == last) ? a.bias_last : a.bias_full;
             const float b1 = (off + 32 == last) ? a.bias_last : a.bias_full;
-            s0[r] += ((blo >> off) & 1u) ? b0 : kNegInf;
-            s1[r] += ((bhi >> off) & 1u) ? b1 : kNegInf;
+            s0[r] += off < nv ? b0 : kNegInf;
+            s1[r] += off + 32 < nv ? b1 : kNegInf;
         }
     };
     // Online softmax in the log2 domain with lazy rescaling, split so that the (rarely
@@ -874,18 +948,20 @@ void routed_attn_kernel(AttnArgs a) {
         exps(s0, s1, pb);
     };
     // O^T += V^T P^T, operands double-buffered in registers.
-    auto pv = [&](auto stage_tag, const f16x8 (&pb)[4]) SOL_INLINE {
+    auto pv = [&](auto apx_tag, auto stage_tag, const f16x8 (&pb)[4]) SOL_INLINE {
+        constexpr bool APX = decltype(apx_tag)::value;
         constexpr int SOFF = decltype(stage_tag)::value * L::STAGE;
+        auto ld = [&](int kk, int mt) SOL_INLINE -> f16x8 {
+            if constexpr (APX) return ldv_apx(kk, mt, SOFF);
+            else return *reinterpret_cast<const f16x8*>(smem + vadr[kk] + SOFF + mt * VMT);
+        };
         f16x8 av[2];
-        av[0] = *reinterpret_cast<const f16x8*>(smem + vadr[0] + SOFF);
+        av[0] = ld(0, 0);
         // kk-major: consecutive MFMAs update different accumulators (no dependent issue)
 #pragma unroll
         for (int i = 0; i < NDT * 4; ++i) {
             const int kk = i / NDT, mt = i % NDT;
-            if (i + 1 < NDT * 4) {
-                const int kk1 = (i + 1) / NDT, mt1 = (i + 1) % NDT;
-                av[(i + 1) & 1] = *reinterpret_cast<const f16x8*>(smem + vadr[kk1] + SOFF + mt1 * VMT);
-            }
+            if (i + 1 < NDT * 4) av[(i + 1) & 1] = ld((i + 1) / NDT, (i + 1) % NDT);
             o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i & 1], pb[kk], o[mt], 0, 0, 0);
         }
     };
@@ -900,9 +976,9 @@ void routed_attn_kernel(AttnArgs a) {
     // runs, then O += V_t P_t.  Stage b's K region holds tile t+1 while its V region still
     // holds tile t, so both stages are busy without a third buffer.  The loop is unrolled by
     // two so that the stage of every LDS access is a compile-time offset.
-    //   correction tiles (sparse mode, list entries [0, napx)): a chunk of f16 pooled keys
-    //     against the f16 query copy, plus the multiplicity bias of each slot;
-    //   exact tiles (list entries [napx, ntiles)): a bf16 key block against the bf16 queries.
+    //   correction tiles (sparse mode, napx of them): 64 gathered unselected routable blocks,
+    //     f16 pooled keys against the f16 query copy plus the multiplicity bias of each slot;
+    //   exact tiles (ntiles of them): a bf16 key block against the bf16 queries.
     // The ragged last key block can only be the final exact tile (it is the last selected or
     // the last forced block), so its mask is applied after the loop.
     auto pipeline = [&](auto apx_tag, const auto& qop, const int T, auto code) SOL_INLINE {
@@ -922,12 +998,7 @@ void routed_attn_kernel(AttnArgs a) {
         };
         // scores of tile t are complete: add the correction bias (correction tiles)
         auto scores_done = [&](int t, f32x16& s0, f32x16& s1) SOL_INLINE {
-            if constexpr (APX) {
-                // keep the selection-word reads (and the biases built from them) here rather
-                // than hoisted across the MFMA slots, where they would hold 32 registers
-                asm volatile("" ::: "memory");
-                bias_apx(code(t), s0, s1);
-            }
+            if constexpr (APX) bias_apx(code(t), s0, s1);
         };
         issue_k(0, 0);
         issue_v(0, 0);
@@ -954,7 +1025,7 @@ void routed_attn_kernel(AttnArgs a) {
             qk(apx_tag, std::integral_constant<int, P ^ 1>{}, qop, n0, n1);
             f16x8 pb[4];
             exps(s0, s1, pb);
-            pv(par_tag, pb);
+            pv(apx_tag, par_tag, pb);
             scores_done(t + 1, n0, n1);
             mx = tile_max(n0, n1);
             __builtin_amdgcn_s_waitcnt(0);
@@ -996,8 +1067,9 @@ void routed_attn_kernel(AttnArgs a) {
             auto ldk = [&](int qi) SOL_INLINE {
                 return *reinterpret_cast<const KT*>(smem + kadr[qi >> 1] + KOFF + (qi & 1) * KT1);
             };
-            auto ldv = [&](int pi) SOL_INLINE {
-                return *reinterpret_cast<const f16x8*>(smem + vadr[pi >> 2] + VOFF + (pi & 3) * VMT);
+            auto ldv = [&](int pi) SOL_INLINE -> f16x8 {
+                if constexpr (APX) return ldv_apx(pi >> 2, pi & 3, VOFF);
+                else return *reinterpret_cast<const f16x8*>(smem + vadr[pi >> 2] + VOFF + (pi & 3) * VMT);
             };
             KT kop[4];
             f16x8 vop[4];
@@ -1050,8 +1122,8 @@ void routed_attn_kernel(AttnArgs a) {
         if constexpr (!APX) mask_tail(code(T - 1), s0, s1);
         f16x8 pb[4];
         softmax(s0, s1, pb);
-        if ((T - 1) & 1) pv(S1{}, pb);
-        else pv(S0{}, pb);
+        if ((T - 1) & 1) pv(apx_tag, S1{}, pb);
+        else pv(apx_tag, S0{}, pb);
     };
 
     if (MODE == kSparse && napx > 0) {
@@ -1062,16 +1134,16 @@ void routed_attn_kernel(AttnArgs a) {
 #pragma unroll
             for (int e = 0; e < 8; ++e) qh[ks][e] = (_Float16)(float)qv[e];
         }
-        pipeline(APX_T{}, qh, napx, [&](int t) SOL_INLINE { return list[t] & ~kApxFlag; });
+        pipeline(APX_T{}, qh, napx, [&](int t) SOL_INLINE { return t; });
         __syncthreads();   // the stages are refilled below while the last V tile may still be read
     }
-    const int T = ntiles - napx;
+    const int T = ntiles;
     if (T > 0) {
         bf16x8 qf[NKS];
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks)
             qf[ks] = qrow < a.N ? *reinterpret_cast<const bf16x8*>(qrow_p + 16 * ks) : bf16x8{};
-        pipeline(EXACT_T{}, qf, T, [&](int t) SOL_INLINE { return tile_code(napx + t); });
+        pipeline(EXACT_T{}, qf, T, [&](int t) SOL_INLINE { return tile_code(t); });
     }
 
     // ---- epilogue: O = O^T / l, bf16
@@ -1124,17 +1196,19 @@ __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
     char* rest = reinterpret_cast<char*>(qt + D * BQ);
     int* scan_scratch = reinterpret_cast<int*>(rest);
     uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64);
-    int* list = reinterpret_cast<int*>(rest + 64 + 4 * ((a.MW + 3) & ~3));
+    uint16_t* list = reinterpret_cast<uint16_t*>(rest + 64 + 4 * ((a.MW + 3) & ~3));
+    const uint16_t* ulist = list;            // correction slots (unselected routable blocks)
+    const uint16_t* elist = list + a.NKr;    // exact tiles
 
     const int bh = blockIdx.y, qi = blockIdx.x, tid = threadIdx.x;
-    int ntiles, nsel, napx = 0;
+    int ntiles, nsel, nuns = 0;
     if (MODE == kDense) {
         ntiles = a.NK;
         nsel = a.NKr;
     } else {
         ntiles = route_and_list<D, NT, MODE>(a.qbar + ((size_t)bh * a.NQ + qi) * D, a.kbar + (size_t)bh * a.NK * D,
                                              a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, selw,
-                                             list, scan_scratch, &napx, &nsel);
+                                             list, scan_scratch, &nuns, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
@@ -1150,17 +1224,19 @@ __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
     for (int c = 0; c < D; ++c) o[c] = 0.f;
     float m = kNegInf, l = 0.f;
 
-    for (int n = 0; n < ntiles; ++n) {
-        const int code = MODE == kDense ? n : list[n];
-        const bool apx = code & kApxFlag;
-        const int c = code & ~kApxFlag;
+    // correction tiles first (64 unselected routable blocks each), then the exact tiles
+    const int napx = MODE == kSparse ? (nuns + kChunk - 1) / kChunk : 0;
+    for (int n = 0; n < napx + ntiles; ++n) {
+        const bool apx = n < napx;
+        const int c = apx ? n : (MODE == kDense ? n : (int)elist[n - napx]);
         __syncthreads();
         for (int e = tid; e < kBlockK * D; e += NT) {
             const int rr = e / D, cc = e % D;
             float kv = 0.f, vv = 0.f;
             if (apx) {
-                const int j = c * kChunk + rr;
-                if (j < a.NKr) {
+                const int u = c * kChunk + rr;
+                if (u < nuns) {
+                    const int j = ulist[u];
                     kv = a.kbar[((size_t)bh * a.NK + j) * D + cc];
                     vv = a.vbar[((size_t)bh * a.NK + j) * D + cc];
                 }
@@ -1178,8 +1254,8 @@ __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
         for (int u = 0; u < kBlockK; ++u) {
             float bias = 0.f;
             if (apx) {
-                const int j = c * kChunk + u;
-                if (j >= a.NKr || ((selw[j >> 5] >> (j & 31)) & 1u)) continue;
+                if (c * kChunk + u >= nuns) continue;
+                const int j = ulist[c * kChunk + u];
                 bias = logf((float)min(kBlockK, a.N - j * kBlockK));
             } else if (c * kBlockK + u >= a.N) {
                 continue;
@@ -1288,7 +1364,7 @@ Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype
 }
 
 size_t attn_lds_bytes(const Shape& s) {
-    const size_t rest = 64 + 4 * (size_t)((s.MW + 3) & ~3) + 4 * (size_t)(s.NK + s.NC);
+    const size_t rest = 64 + 4 * (size_t)((s.MW + 3) & ~3) + 2 * (size_t)(s.NKr + s.NK);
     if (s.dtype == kBF16) {
         const size_t stage = (size_t)kBlockK * s.d * 2 * 2;
         return 2 * stage + rest;
@@ -1318,7 +1394,7 @@ size_t workspace_layout(const Shape& s, char* base, Workspace* ws) {
         w.vt = reinterpret_cast<_Float16*>(take(BH * d * (size_t)s.Npad * 2));
         if (routing) {
             w.kbarh = reinterpret_cast<_Float16*>(take(BH * (size_t)s.NC * kChunk * d * 2));
-            w.vbart = reinterpret_cast<_Float16*>(take(BH * (size_t)s.NC * d * kChunk * 2));
+            w.vbarh = reinterpret_cast<_Float16*>(take(BH * (size_t)s.NC * kChunk * d * 2));
         }
     } else if (s.mode == kSparse) {
         w.vbar = reinterpret_cast<float*>(take(BH * s.NK * d * 4));
@@ -1376,10 +1452,10 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         const uint16_t* kk = static_cast<const uint16_t*>(k);
         const uint16_t* vv = static_cast<const uint16_t*>(v);
         if (d == 128)
-            prep_kv_kernel<128><<<dim3(nj, s.BH), dim3(256), 0, st>>>(kk, vv, ws.kbar, ws.kbarh, ws.vbart, ws.vt, s.N,
+            prep_kv_kernel<128><<<dim3(nj, s.BH), dim3(256), 0, st>>>(kk, vv, ws.kbar, ws.kbarh, ws.vbarh, ws.vt, s.N,
                                                                       s.NK, s.NKr, s.NC, routing ? 1 : 0);
         else
-            prep_kv_kernel<64><<<dim3(nj, s.BH), dim3(256), 0, st>>>(kk, vv, ws.kbar, ws.kbarh, ws.vbart, ws.vt, s.N,
+            prep_kv_kernel<64><<<dim3(nj, s.BH), dim3(256), 0, st>>>(kk, vv, ws.kbar, ws.kbarh, ws.vbarh, ws.vt, s.N,
                                                                      s.NK, s.NKr, s.NC, routing ? 1 : 0);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (routing) {
@@ -1394,7 +1470,7 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         a.qbar = ws.qbar;
         a.kbar = ws.kbar;
         a.kbarh = ws.kbarh;
-        a.vbart = ws.vbart;
+        a.vbarh = ws.vbarh;
         a.tau = ws.tau;
         a.out = static_cast<uint16_t*>(out);
         a.blkcount = ws.blkcount;
