@@ -42,6 +42,7 @@ from typing import Optional, Sequence
 import numpy as np
 
 MODES = ("dense", "sparse", "sparse_no_correction")
+THRESHOLD_MODES = ("exact", "diagonal")
 BAND = 1e-3
 
 
@@ -97,7 +98,9 @@ def row_stats_from_moments(qbar: np.ndarray, kbar: np.ndarray, scale: float):
 
 
 def diagonal_sigma(qbar: np.ndarray, kbar: np.ndarray, scale: float):
-    """Diagonal-covariance estimate of sigma_i (Appendix, Eq. appendix_diagonal_threshold)."""
+    """Diagonal-covariance estimate of sigma_i (Appendix, Eq. appendix_diagonal_threshold):
+    v_K = mean_j(Kbar_j * Kbar_j) - mu_K * mu_K over the pooled keys given (the routable
+    ones), sigma_i^2 = scale^2 * (Qbar_i * Qbar_i) . v_K."""
     mean_k = kbar.mean(axis=-2)
     v_k = (kbar * kbar).mean(axis=-2) - mean_k * mean_k
     var = scale * scale * ((qbar * qbar) @ v_k[..., None])[..., 0]
@@ -139,7 +142,7 @@ def approx_terms(q_rows, kbar_blocks, vhat_blocks, counts, scale, shift):
 
 
 def _forward_head(args):
-    (qh, kh, vh, block_q, block_k, beta, mode, n_forced, qblocks, mask_h) = args
+    (qh, kh, vh, block_q, block_k, beta, mode, n_forced, qblocks, mask_h, threshold_mode) = args
     qh = np.asarray(qh, dtype=np.float64)
     kh = np.asarray(kh, dtype=np.float64)
     vh = np.asarray(vh, dtype=np.float64)
@@ -153,6 +156,8 @@ def _forward_head(args):
 
     s_hat = proxy_scores(qbar, kbar[:nkr], scale)
     mu, sigma = row_stats(s_hat)
+    if threshold_mode == "diagonal":
+        sigma = diagonal_sigma(qbar, kbar[:nkr], scale)
     tau = thresholds(mu, sigma, beta)
     sel = route(s_hat, tau) if mask_h is None else np.asarray(mask_h, dtype=bool)
     band = int(np.count_nonzero(np.abs(s_hat - tau[:, None]) < BAND))
@@ -197,7 +202,7 @@ def _forward_head(args):
 def forward(q, k, v, block_q: int, block_k: int, beta: float, mode: str,
             keep_tail_tokens: int = 0, query_blocks: Optional[Sequence[int]] = None,
             mask: Optional[np.ndarray] = None, heads: Optional[Sequence] = None,
-            workers: int = 0) -> dict:
+            workers: int = 0, threshold_mode: str = "exact") -> dict:
     """Sol-Attn forward pass for q, k, v of shape [B, H, N, d].
 
     mode: "dense" (Eq. dense_attn), "sparse" (exact selected blocks plus the
@@ -207,6 +212,8 @@ def forward(q, k, v, block_q: int, block_k: int, beta: float, mode: str,
     query_blocks: optional subset of query blocks to evaluate (other rows NaN).
     mask: optional [B, H, NQ, NK_routable] selection to use instead of routing.
     heads: optional list of (b, h) to evaluate (other heads NaN / empty).
+    threshold_mode: "exact" (sigma_i from the full proxy row, equal to Eq.
+    threshold_stats_exact) or "diagonal" (Appendix, Eq. appendix_diagonal_threshold).
 
     Returns a dict with out [B,H,N,d] float64, mask [B,H,NQ,NKr] bool, s_hat, tau,
     mu, sigma, frac [B,H] (kept fraction of routable pairs; 1.0 for dense) and
@@ -214,6 +221,8 @@ def forward(q, k, v, block_q: int, block_k: int, beta: float, mode: str,
     """
     if mode not in MODES:
         raise ValueError(f"mode must be one of {MODES}")
+    if threshold_mode not in THRESHOLD_MODES:
+        raise ValueError(f"threshold_mode must be one of {THRESHOLD_MODES}")
     q = np.asarray(q)
     k = np.asarray(k)
     v = np.asarray(v)
@@ -228,7 +237,7 @@ def forward(q, k, v, block_q: int, block_k: int, beta: float, mode: str,
     head_list = [(b, h) for b in range(B) for h in range(H)] if heads is None else list(heads)
 
     jobs = [(q[b, h], k[b, h], v[b, h], block_q, block_k, beta, mode, n_forced, qblocks,
-             None if mask is None else mask[b, h]) for b, h in head_list]
+             None if mask is None else mask[b, h], threshold_mode) for b, h in head_list]
     if workers and workers > 1 and len(jobs) > 1:
         with ProcessPoolExecutor(max_workers=min(workers, len(jobs))) as ex:
             results = list(ex.map(_forward_head, jobs))
@@ -257,7 +266,8 @@ def forward(q, k, v, block_q: int, block_k: int, beta: float, mode: str,
     return res
 
 
-def routing(q, k, block_q: int, block_k: int, beta: float, keep_tail_tokens: int = 0) -> dict:
+def routing(q, k, block_q: int, block_k: int, beta: float, keep_tail_tokens: int = 0,
+            threshold_mode: str = "exact") -> dict:
     """Routing only (pool -> proxies -> row statistics -> thresholds -> mask) for
     all heads; cheap enough for the full 720p map."""
     q = np.asarray(q)
@@ -270,6 +280,8 @@ def routing(q, k, block_q: int, block_k: int, beta: float, keep_tail_tokens: int
     nkr = kbar.shape[-2] - n_forced
     s_hat = proxy_scores(qbar, kbar[..., :nkr, :], scale)
     mu, sigma = row_stats(s_hat)
+    if threshold_mode == "diagonal":
+        sigma = diagonal_sigma(qbar, kbar[..., :nkr, :], scale)
     tau = thresholds(mu, sigma, beta)
     sel = route(s_hat, tau)
     band = np.count_nonzero(np.abs(s_hat - tau[..., None]) < BAND, axis=(-1, -2))

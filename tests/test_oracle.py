@@ -119,6 +119,69 @@ def test_chunked_thresholding_recovers_full_row_set():
         assert np.array_equal(sel, r["mask"])
 
 
+def hadamard(n):
+    h = np.array([[1.0]])
+    while h.shape[0] < n:
+        h = np.block([[h, h], [h, -h]])
+    return h
+
+
+def test_diagonal_threshold_equals_exact_for_uncorrelated_pooled_keys():
+    # Appendix, Eq. appendix_diagonal_threshold keeps only the diagonal of the
+    # pooled-key covariance.  Block keys built from the columns of a Hadamard
+    # matrix (orthogonal, zero-mean except the constant first column) have an
+    # exactly diagonal covariance, so the diagonal estimate must equal the exact
+    # standard deviation of the materialised proxy row.
+    rng = np.random.default_rng(40)
+    d, bk, bq = 16, 4, 8
+    colscale = rng.uniform(0.5, 2.0, d)
+    kbar = hadamard(d) * colscale                       # 16 blocks x 16 dims
+    k = np.repeat(kbar, bk, axis=0)[None, None]         # block-constant keys
+    q = rng.standard_normal((1, 1, 6 * bq, d))
+    ex = ora.routing(q, k, bq, bk, 0.7)
+    dg = ora.routing(q, k, bq, bk, 0.7, threshold_mode="diagonal")
+    assert np.max(np.abs(dg["sigma"] - ex["sigma"])) < 1e-12
+    assert np.array_equal(dg["mask"], ex["mask"])
+
+
+def test_diagonal_threshold_brute_force():
+    # sigma_i^2 = s^2 * sum_d Qbar_id^2 * (1/N) sum_j (Kbar_jd - mean_d)^2, written
+    # out with plain loops on a tiny case.
+    rng = np.random.default_rng(41)
+    d, bk, bq, n = 6, 4, 5, 37
+    q = rng.standard_normal((1, 1, n, d))
+    k = rng.standard_normal((1, 1, n, d)) + rng.standard_normal(d)
+    r = ora.routing(q, k, bq, bk, 0.3, threshold_mode="diagonal")
+    qh, kh = q[0, 0], k[0, 0]
+    kb = [[sum(kh[t, c] for t in range(j, min(j + bk, n))) / (min(j + bk, n) - j) for c in range(d)]
+          for j in range(0, n, bk)]
+    nk = len(kb)
+    mean = [sum(kb[j][c] for j in range(nk)) / nk for c in range(d)]
+    var = [sum((kb[j][c] - mean[c]) ** 2 for j in range(nk)) / nk for c in range(d)]
+    s = 1 / math.sqrt(d)
+    for i, i0 in enumerate(range(0, n, bq)):
+        rows = range(i0, min(i0 + bq, n))
+        qb = [sum(qh[t, c] for t in rows) / len(rows) for c in range(d)]
+        sig = math.sqrt(s * s * sum(qb[c] ** 2 * var[c] for c in range(d)))
+        assert abs(r["sigma"][0, 0, i] - sig) < 1e-12
+        mu = s * sum(qb[c] * mean[c] for c in range(d))
+        assert abs(r["tau"][0, 0, i] - (mu + 0.3 * sig)) < 1e-12
+
+
+def test_diagonal_threshold_differs_for_correlated_keys():
+    # With two perfectly correlated key dimensions the off-diagonal covariance is
+    # large, and dropping it must change sigma (the flag is not a no-op).
+    rng = np.random.default_rng(42)
+    d, bk = 8, 4
+    base = rng.standard_normal((64, 1))
+    kbar = np.concatenate([base, base, 0.1 * rng.standard_normal((64, d - 2))], axis=1)
+    k = np.repeat(kbar, bk, axis=0)[None, None]
+    q = np.ones((1, 1, 16, d))
+    ex = ora.routing(q, k, 8, bk, 0.5)
+    dg = ora.routing(q, k, 8, bk, 0.5, threshold_mode="diagonal")
+    assert np.min(np.abs(dg["sigma"] - ex["sigma"]) / ex["sigma"]) > 0.2
+
+
 @pytest.mark.parametrize("beta", [0.0, 0.5, 1.0, 1.5])
 def test_kept_density_follows_gaussian_tail(beta):
     # Keys constant within each block with iid N(0, I) block values make every
@@ -377,6 +440,19 @@ def test_pins_catch_a_dropped_multiplicity(monkeypatch):
     monkeypatch.setattr(ora, "approx_terms", wrong)
     res = ora.forward(q, k, v, 32, 16, 0.5, "sparse")
     assert np.max(np.abs(res["out"] - 1.0)) > 1e-2
+
+
+def test_pins_catch_an_uncentred_diagonal_estimate(monkeypatch):
+    # A plausible slip in Eq. appendix_diagonal_threshold (forgetting to subtract
+    # mu_K * mu_K) must break the uncorrelated-keys pin: the constant Hadamard
+    # column then contributes.
+    def wrong(qbar, kbar, scale):
+        v_k = (kbar * kbar).mean(axis=-2)
+        return np.sqrt(scale * scale * ((qbar * qbar) @ v_k[..., None])[..., 0])
+
+    monkeypatch.setattr(ora, "diagonal_sigma", wrong)
+    with pytest.raises(AssertionError):
+        test_diagonal_threshold_equals_exact_for_uncorrelated_pooled_keys()
 
 
 def test_pins_catch_a_flipped_threshold_sign():
