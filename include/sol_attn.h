@@ -38,6 +38,14 @@ enum {
     SOL_SPARSE_NO_CORRECTION = 2  /* routed exact blocks only (Section 2, Eq. block_sparse_attn) */
 };
 
+/* Threshold estimator flag, OR-ed into `mode` of the forward calls and of
+ * sol_attn_workspace_bytes (ignored by SOL_DENSE), or passed as the
+ * threshold_mode of sol_attn_thresholds.  Without it sigma_i uses the full
+ * pooled-key covariance (Eq. threshold_stats_exact); with it only the diagonal
+ * v_K = mean_j(Kbar_j * Kbar_j) - mu_K * mu_K, sigma_i^2 = s^2 (Qbar_i * Qbar_i) . v_K
+ * (Appendix, "Diagonal threshold estimator", Eq. appendix_diagonal_threshold). */
+enum { SOL_THRESHOLD_DIAGONAL = 0x100 };
+
 /* Element types of q, k, v and out. */
 enum { SOL_BF16 = 0, SOL_F32 = 1 };
 
@@ -79,20 +87,22 @@ int sol_attn_pool_blocks(const void* q, const void* k, const void* v,
  *
  * qbar: [B,H,NQ,d] f32 device; kbar: [B,H,NK,d] f32 device (NK >= nk_routable,
  * row stride d, NK rows per (b,h)).  tau (required), mu, sigma (optional):
- * [B,H,NQ] f32 device.  beta must not be NaN.  Unlike the forward calls this
- * entry point allocates temporary device memory for the moments and
- * synchronises `stream` before returning.
+ * [B,H,NQ] f32 device.  beta must not be NaN.  threshold_mode: 0 (exact) or
+ * SOL_THRESHOLD_DIAGONAL.  Unlike the forward calls this entry point allocates
+ * temporary device memory for the moments and synchronises `stream` before
+ * returning.
  */
 int sol_attn_thresholds(const float* qbar, const float* kbar,
                         float* tau, float* mu, float* sigma,
                         int B, int H, int NQ, int NK, int nk_routable, int d,
-                        float beta, void* stream);
+                        float beta, int threshold_mode, void* stream);
 
 /*
  * Routed attention forward, short form: bf16 q/k/v/out, default stream,
  * library-managed workspace, per-head counts kept for sol_attn_stats().
  * `tau` is the standardised cutoff beta of Eq. threshold_routing; mode is one
- * of SOL_DENSE, SOL_SPARSE, SOL_SPARSE_NO_CORRECTION.
+ * of SOL_DENSE, SOL_SPARSE, SOL_SPARSE_NO_CORRECTION, optionally OR-ed with
+ * SOL_THRESHOLD_DIAGONAL.
  */
 int sol_attn_forward(const void* q, const void* k, const void* v, void* out,
                      int B, int H, int N, int d, int block_q, int block_k,
@@ -120,6 +130,8 @@ int sol_attn_forward(const void* q, const void* k, const void* v, void* out,
  * mask_out: [B,H,NQ,ceil(NKr/32)] u32 device bit mask of the selection (bit
  *   j%32 of word j/32 for key block j), or NULL.  Debug/parity aid; not
  *   written in SOL_DENSE.
+ * mode: SOL_DENSE, SOL_SPARSE or SOL_SPARSE_NO_CORRECTION, optionally OR-ed with
+ *   SOL_THRESHOLD_DIAGONAL (any other bit is an error).
  * stream: hipStream_t or NULL.
  *
  * Selection is computed on chip from f32 pooled proxies s*Qbar_i.Kbar_j and

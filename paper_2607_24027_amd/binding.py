@@ -17,6 +17,8 @@ LIB_PATH = os.path.join(HERE, "libsolattn.so")
 
 SOL_DENSE, SOL_SPARSE, SOL_SPARSE_NO_CORRECTION = 0, 1, 2
 SOL_BF16, SOL_F32 = 0, 1
+SOL_THRESHOLD_DIAGONAL = 0x100
+THRESHOLD_MODES = {"exact": 0, "diagonal": SOL_THRESHOLD_DIAGONAL}
 SOL_OK, SOL_ERR_INVALID_ARG, SOL_ERR_UNSUPPORTED, SOL_ERR_HIP, SOL_ERR_WORKSPACE, SOL_ERR_NO_DATA = 0, -1, -2, -3, -4, -5
 MODES = {"dense": SOL_DENSE, "sparse": SOL_SPARSE, "sparse_no_correction": SOL_SPARSE_NO_CORRECTION}
 
@@ -24,7 +26,7 @@ MODES = {"dense": SOL_DENSE, "sparse": SOL_SPARSE, "sparse_no_correction": SOL_S
 _P, _I, _F, _S = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
 SIGNATURES = {
     "sol_attn_pool_blocks": (_I, [_P, _P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _P]),
-    "sol_attn_thresholds": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _P]),
+    "sol_attn_thresholds": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _P]),
     "sol_attn_forward": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I]),
     "sol_attn_forward_ex": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _I, _I, _P, _S, _P, _P, _P]),
     "sol_attn_workspace_bytes": (_S, [_I, _I, _I, _I, _I, _I, _I, _I, _I]),
@@ -108,8 +110,9 @@ def pool_blocks(q, k, v, block_q: int, block_k: int):
     return qbar, kbar, vbar
 
 
-def thresholds(qbar, kbar, beta: float, nk_routable: Optional[int] = None):
-    """(tau, mu, sigma) [B,H,NQ] f32 from pooled queries/keys (moment form)."""
+def thresholds(qbar, kbar, beta: float, nk_routable: Optional[int] = None, threshold_mode: str = "exact"):
+    """(tau, mu, sigma) [B,H,NQ] f32 from pooled queries/keys (moment form, or the
+    diagonal estimator with threshold_mode="diagonal")."""
     import torch
     B, H, NQ, d = qbar.shape
     NK = kbar.shape[2]
@@ -118,8 +121,13 @@ def thresholds(qbar, kbar, beta: float, nk_routable: Optional[int] = None):
     mu = torch.empty_like(tau)
     sigma = torch.empty_like(tau)
     _check(lib().sol_attn_thresholds(_ptr(qbar.contiguous()), _ptr(kbar.contiguous()), _ptr(tau), _ptr(mu),
-                                     _ptr(sigma), B, H, NQ, NK, nkr, d, float(beta), _stream(qbar.device)))
+                                     _ptr(sigma), B, H, NQ, NK, nkr, d, float(beta),
+                                     THRESHOLD_MODES[threshold_mode], _stream(qbar.device)))
     return tau, mu, sigma
+
+
+def _mode_code(mode, threshold_mode="exact") -> int:
+    return (MODES[mode] if isinstance(mode, str) else int(mode)) | THRESHOLD_MODES[threshold_mode]
 
 
 def workspace_bytes(B, H, N, d, block_q, block_k, mode, dtype=SOL_BF16, keep_tail_tokens=0) -> int:
@@ -128,14 +136,15 @@ def workspace_bytes(B, H, N, d, block_q, block_k, mode, dtype=SOL_BF16, keep_tai
 
 
 def forward(q, k, v, block_q: int, block_k: int, tau: float, mode="sparse", keep_tail_tokens: int = 0,
-            out=None, workspace=None, counts=None, mask_out=None):
-    """Routed attention forward through sol_attn_forward_ex.  Returns out."""
+            out=None, workspace=None, counts=None, mask_out=None, threshold_mode: str = "exact"):
+    """Routed attention forward through sol_attn_forward_ex.  Returns out.
+    threshold_mode "diagonal" ORs SOL_THRESHOLD_DIAGONAL into the mode."""
     import torch
     _check_qkv(q, k, v)
     B, H, N, d = q.shape
     if out is None:
         out = torch.empty_like(q)
-    m = MODES[mode] if isinstance(mode, str) else int(mode)
+    m = _mode_code(mode, threshold_mode)
     ws_ptr, ws_bytes = (None, 0) if workspace is None else (workspace.data_ptr(), workspace.numel() * workspace.element_size())
     _check(lib().sol_attn_forward_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, block_q, block_k,
                                      float(tau), m, _dtype_code(q), keep_tail_tokens, ws_ptr, ws_bytes,

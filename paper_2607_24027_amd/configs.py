@@ -78,11 +78,12 @@ def load_betas() -> dict:
         return {}
 
 
-def beta_for(workload: Workload, kept: Optional[float] = None) -> float:
+def beta_for(workload: Workload, kept: Optional[float] = None, threshold_mode: str = "exact") -> float:
+    """Calibrated cutoff for a kept fraction, for the exact or the diagonal threshold estimator."""
     kept = workload.target_kept if kept is None else kept
     if kept >= 1.0:
         return float("-inf")
-    key = f"{workload.name}@{kept:.2f}"
+    key = f"{workload.name}@{kept:.2f}" + ("" if threshold_mode == "exact" else f"/{threshold_mode}")
     betas = load_betas()
     if key not in betas:
         raise KeyError(f"no calibrated beta for {key}; run oracle/calibrate_beta.py")

@@ -84,13 +84,16 @@ int validate_forward(const void* q, const void* k, const void* v, const void* ou
     if (!q || !k || !v || !out) return fail(SOL_ERR_INVALID_ARG, "q, k, v and out must be non-null");
     int rc = check_common(B, H, N, d, block_q, block_k, dtype);
     if (rc) return rc;
-    if (mode != SOL_DENSE && mode != SOL_SPARSE && mode != SOL_SPARSE_NO_CORRECTION)
-        return fail(SOL_ERR_INVALID_ARG, "mode must be SOL_DENSE, SOL_SPARSE or SOL_SPARSE_NO_CORRECTION (got %d)", mode);
+    const int base = mode & ~SOL_THRESHOLD_DIAGONAL;
+    if (base != SOL_DENSE && base != SOL_SPARSE && base != SOL_SPARSE_NO_CORRECTION)
+        return fail(SOL_ERR_INVALID_ARG,
+                    "mode must be SOL_DENSE, SOL_SPARSE or SOL_SPARSE_NO_CORRECTION, optionally | SOL_THRESHOLD_DIAGONAL "
+                    "(got %d)", mode);
     if (!finite_or_inf(tau)) return fail(SOL_ERR_INVALID_ARG, "tau (standardised cutoff beta) is NaN");
     if (block_k != 64) return fail(SOL_ERR_UNSUPPORTED, "block_k must be 64 (got %d)", block_k);
     if (block_q != 64 && block_q != 128) return fail(SOL_ERR_UNSUPPORTED, "block_q must be 64 or 128 (got %d)", block_q);
     if (keep_tail < 0 || keep_tail % block_k) return fail(SOL_ERR_INVALID_ARG, "keep_tail_tokens must be a non-negative multiple of block_k (got %d)", keep_tail);
-    if (keep_tail >= N && mode != SOL_DENSE) return fail(SOL_ERR_INVALID_ARG, "keep_tail_tokens must leave at least one routable key block");
+    if (keep_tail >= N && base != SOL_DENSE) return fail(SOL_ERR_INVALID_ARG, "keep_tail_tokens must leave at least one routable key block");
     if (keep_tail > N) return fail(SOL_ERR_INVALID_ARG, "keep_tail_tokens exceeds N");
     if (out == q || out == k || out == v) return fail(SOL_ERR_INVALID_ARG, "out must not alias q, k or v");
     const sol::Shape s = sol::make_shape(B, H, N, d, block_q, block_k, mode, dtype, keep_tail);
@@ -122,12 +125,14 @@ int sol_attn_pool_blocks(const void* q, const void* k, const void* v, float* qba
 }
 
 int sol_attn_thresholds(const float* qbar, const float* kbar, float* tau, float* mu, float* sigma, int B, int H, int NQ,
-                        int NK, int nk_routable, int d, float beta, void* stream) {
+                        int NK, int nk_routable, int d, float beta, int threshold_mode, void* stream) {
     if (!qbar || !kbar || !tau) return fail(SOL_ERR_INVALID_ARG, "qbar, kbar and tau must be non-null");
     if (B <= 0 || H <= 0 || NQ <= 0 || NK <= 0) return fail(SOL_ERR_INVALID_ARG, "B, H, NQ and NK must be positive");
     if (nk_routable <= 0 || nk_routable > NK) return fail(SOL_ERR_INVALID_ARG, "nk_routable must be in [1, NK]");
     if (d != 64 && d != 128) return fail(SOL_ERR_UNSUPPORTED, "d must be 64 or 128 (got %d)", d);
     if (std::isnan(beta)) return fail(SOL_ERR_INVALID_ARG, "beta is NaN");
+    if (threshold_mode != 0 && threshold_mode != SOL_THRESHOLD_DIAGONAL)
+        return fail(SOL_ERR_INVALID_ARG, "threshold_mode must be 0 or SOL_THRESHOLD_DIAGONAL (got %d)", threshold_mode);
     hipStream_t st = static_cast<hipStream_t>(stream);
     const int BH = B * H;
     // Moment buffers are temporary: allocate, run, wait, free (this entry point synchronises).
@@ -139,7 +144,8 @@ int sol_attn_thresholds(const float* qbar, const float* kbar, float* tau, float*
     float* cov = reinterpret_cast<float*>(static_cast<char*>(mom) + part);
     float* muk = cov + (size_t)BH * d * d;
     e = sol::launch_moments(kbar, muk, cov, scratch, BH, NK, nk_routable, d, st);
-    if (e == hipSuccess) e = sol::launch_tau(qbar, muk, cov, tau, mu, sigma, BH, NQ, d, beta, st);
+    if (e == hipSuccess) e = sol::launch_tau(qbar, muk, cov, tau, mu, sigma, BH, NQ, d, beta,
+                                                    threshold_mode == SOL_THRESHOLD_DIAGONAL ? 1 : 0, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
     (void)hipFree(mom);
     if (e != hipSuccess) return hip_fail(e, "threshold kernels");

@@ -14,15 +14,18 @@ constexpr int kChunk = 64;         // pooled keys per correction tile
 constexpr int kMaxLds = 160 * 1024;
 
 enum Mode { kDense = 0, kSparse = 1, kSparseNoCorr = 2 };
+constexpr int kThresholdDiagonal = 0x100;   // flag bit of the ABI mode (SOL_THRESHOLD_DIAGONAL)
 enum DType { kBF16 = 0, kF32 = 1 };
 
 // Derived sizes of one forward call.
 struct Shape {
     int B, H, N, d, bq, bk;
     int mode, dtype, forced;       // forced = number of always-exact tail key blocks
+    int diag;                      // 1: diagonal threshold estimator
     int BH, NQ, NK, NKr, NC, Npad, MW;
 };
 
+// `mode` is the ABI mode: base mode plus optional kThresholdDiagonal.
 Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype, int keep_tail_tokens);
 
 // Workspace carve-up (all device pointers, 256-byte aligned inside one buffer).
@@ -52,7 +55,7 @@ size_t moments_scratch_bytes(int BH, int d);
 hipError_t launch_moments(const float* kbar, float* muk, float* cov, double* scratch, int BH, int NK, int NKr,
                           int d, hipStream_t st);
 hipError_t launch_tau(const float* qbar, const float* muk, const float* cov, float* tau, float* mu,
-                      float* sigma, int BH, int NQ, int d, float beta, hipStream_t st);
+                      float* sigma, int BH, int NQ, int d, float beta, int diag, hipStream_t st);
 // ev_start/ev_stop (nullable) are recorded on `st` around the fused attention kernel.
 hipError_t launch_forward(const Shape& s, const void* q, const void* k, const void* v, void* out,
                           float beta, const Workspace& ws, uint32_t* counts, uint32_t* mask_out,

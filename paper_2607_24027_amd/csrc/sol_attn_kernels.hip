@@ -319,14 +319,15 @@ __global__ __launch_bounds__(256) void moments_final_kernel(const float* __restr
 }
 
 // ---------------------------------------------------------------------------
-// Thresholds (Eq. threshold_routing with Eq. threshold_stats_exact).  grid (ceil(NQ/16), BH),
+// Thresholds (Eq. threshold_routing with Eq. threshold_stats_exact, or with the diagonal
+// estimator of the Appendix, Eq. appendix_diagonal_threshold, when DIAG).  grid (ceil(NQ/16), BH),
 // 256 threads in 256/D groups of D.  Thread (g, r) holds column r of C_K (= row r, C_K is
 // symmetric) in registers and, for the group's query blocks i, forms y_r = (C_K Qbar_i^T)_r
 // from the staged Qbar rows (broadcast LDS reads); the D products Qbar_ir y_r and
 // Qbar_ir mu_r are summed per wave, and the wave partials per query block give
 // Qbar_i C_K Qbar_i^T and Qbar_i mu_K^T.
 // ---------------------------------------------------------------------------
-template <int D>
+template <int D, bool DIAG>
 __global__ __launch_bounds__(256) void tau_kernel(const float* __restrict__ qbar, const float* __restrict__ muk,
                                                   const float* __restrict__ cov, float* __restrict__ tau,
                                                   float* __restrict__ mu_out, float* __restrict__ sigma_out,
@@ -339,24 +340,34 @@ __global__ __launch_bounds__(256) void tau_kernel(const float* __restrict__ qbar
     const int bh = blockIdx.y, i0 = blockIdx.x * QPB, t = threadIdx.x;
     const int nq = min(QPB, NQ - i0);
     const int g = t / D, r = t % D, wv = r / 64, lane = t & 63;
-    float ccol[D];
+    float ccol[DIAG ? 1 : D];
+    if constexpr (DIAG) {
+        ccol[0] = cov[((size_t)bh * D + r) * D + r];   // v_K[r], the diagonal of C_K
+    } else {
 #pragma unroll
-    for (int c = 0; c < D; ++c) ccol[c] = cov[((size_t)bh * D + c) * D + r];
+        for (int c = 0; c < D; ++c) ccol[c] = cov[((size_t)bh * D + c) * D + r];
+    }
     const float mkr = muk[(size_t)bh * D + r];
     for (int e = t; e < nq * D; e += 256) qs[e] = qbar[((size_t)bh * NQ + i0) * D + e];
     __syncthreads();
     for (int qq = g; qq < nq; qq += PAR) {
         const float* qrow = qs + qq * D;
-        float y0 = 0.f, y1 = 0.f;
+        float y;
+        if constexpr (DIAG) {
+            y = ccol[0] * qrow[r];   // (diag(v_K) Qbar_i^T)_r
+        } else {
+            float y0 = 0.f, y1 = 0.f;
 #pragma unroll
-        for (int c = 0; c < D; c += 4) {
-            const f32x4 qv = *reinterpret_cast<const f32x4*>(qrow + c);
-            y0 = fmaf(ccol[c], qv[0], y0);
-            y1 = fmaf(ccol[c + 1], qv[1], y1);
-            y0 = fmaf(ccol[c + 2], qv[2], y0);
-            y1 = fmaf(ccol[c + 3], qv[3], y1);
+            for (int c = 0; c < D; c += 4) {
+                const f32x4 qv = *reinterpret_cast<const f32x4*>(qrow + c);
+                y0 = fmaf(ccol[c], qv[0], y0);
+                y1 = fmaf(ccol[c + 1], qv[1], y1);
+                y0 = fmaf(ccol[c + 2], qv[2], y0);
+                y1 = fmaf(ccol[c + 3], qv[3], y1);
+            }
+            y = y0 + y1;
         }
-        float w = qrow[r] * (y0 + y1);
+        float w = qrow[r] * y;
         float m = qrow[r] * mkr;
 #pragma unroll
         for (int off = 32; off > 0; off >>= 1) {
@@ -1351,7 +1362,8 @@ hipError_t dispatch_f32_mode(const Shape& s, const AttnArgsF32& a, hipStream_t s
 Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype, int keep_tail_tokens) {
     Shape s{};
     s.B = B; s.H = H; s.N = N; s.d = d; s.bq = bq; s.bk = bk;
-    s.mode = mode; s.dtype = dtype;
+    s.mode = mode & ~kThresholdDiagonal; s.dtype = dtype;
+    s.diag = (mode & kThresholdDiagonal) ? 1 : 0;
     s.forced = bk > 0 ? keep_tail_tokens / bk : 0;
     s.BH = B * H;
     s.NQ = bq > 0 ? (N + bq - 1) / bq : 0;
@@ -1428,11 +1440,16 @@ hipError_t launch_moments(const float* kbar, float* muk, float* cov, double* scr
 }
 
 hipError_t launch_tau(const float* qbar, const float* muk, const float* cov, float* tau, float* mu, float* sigma,
-                      int BH, int NQ, int d, float beta, hipStream_t st) {
+                      int BH, int NQ, int d, float beta, int diag, hipStream_t st) {
     const float scale = 1.0f / sqrtf((float)d);
     const dim3 grid((NQ + 15) / 16, BH);
-    if (d == 128) tau_kernel<128><<<grid, dim3(256), 0, st>>>(qbar, muk, cov, tau, mu, sigma, NQ, beta, scale);
-    else tau_kernel<64><<<grid, dim3(256), 0, st>>>(qbar, muk, cov, tau, mu, sigma, NQ, beta, scale);
+    if (d == 128) {
+        if (diag) tau_kernel<128, true><<<grid, dim3(256), 0, st>>>(qbar, muk, cov, tau, mu, sigma, NQ, beta, scale);
+        else tau_kernel<128, false><<<grid, dim3(256), 0, st>>>(qbar, muk, cov, tau, mu, sigma, NQ, beta, scale);
+    } else {
+        if (diag) tau_kernel<64, true><<<grid, dim3(256), 0, st>>>(qbar, muk, cov, tau, mu, sigma, NQ, beta, scale);
+        else tau_kernel<64, false><<<grid, dim3(256), 0, st>>>(qbar, muk, cov, tau, mu, sigma, NQ, beta, scale);
+    }
     return hipGetLastError();
 }
 
@@ -1460,7 +1477,7 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (routing) {
             if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, ws.mom, s.BH, s.NK, s.NKr, d, st)) != hipSuccess) return e;
-            if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, st)) != hipSuccess)
+            if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, s.diag, st)) != hipSuccess)
                 return e;
         }
         AttnArgs a{};
@@ -1493,7 +1510,7 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
             if (s.mode == kSparse && (e = launch_pool_mean(v, ws.vbar, kF32, s.BH, s.N, d, s.bk, st)) != hipSuccess)
                 return e;
             if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, ws.mom, s.BH, s.NK, s.NKr, d, st)) != hipSuccess) return e;
-            if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, st)) != hipSuccess)
+            if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, s.diag, st)) != hipSuccess)
                 return e;
         }
         AttnArgsF32 a{};

@@ -32,10 +32,11 @@ def test_library_exports_every_declared_symbol():
 def test_header_constants_match_binding():
     text = open(HEADER).read()
     for name, val in [("SOL_DENSE", 0), ("SOL_SPARSE", 1), ("SOL_SPARSE_NO_CORRECTION", 2), ("SOL_BF16", 0),
+                      ("SOL_THRESHOLD_DIAGONAL", 0x100),
                       ("SOL_F32", 1), ("SOL_ERR_INVALID_ARG", -1), ("SOL_ERR_UNSUPPORTED", -2),
                       ("SOL_ERR_HIP", -3), ("SOL_ERR_WORKSPACE", -4), ("SOL_ERR_NO_DATA", -5)]:
-        m = re.search(rf"\b{name}\s*=\s*(-?\d+)", text)
-        assert m and int(m.group(1)) == val
+        m = re.search(rf"\b{name}\s*=\s*(-?(?:0x[0-9a-fA-F]+|\d+))", text)
+        assert m and int(m.group(1), 0) == val
         assert getattr(sb, name) == val
 
 
@@ -52,6 +53,8 @@ def fwd(*, B=1, H=2, N=1000, d=128, bq=128, bk=64, tau=0.5, mode=1, dtype=0, kee
     (dict(N=0), sb.SOL_ERR_INVALID_ARG),
     (dict(B=-1), sb.SOL_ERR_INVALID_ARG),
     (dict(mode=7), sb.SOL_ERR_INVALID_ARG),
+    (dict(mode=sb.SOL_SPARSE | 0x200), sb.SOL_ERR_INVALID_ARG),
+    (dict(mode=3 | sb.SOL_THRESHOLD_DIAGONAL), sb.SOL_ERR_INVALID_ARG),
     (dict(dtype=5), sb.SOL_ERR_INVALID_ARG),
     (dict(tau=float("nan")), sb.SOL_ERR_INVALID_ARG),
     (dict(keep=30), sb.SOL_ERR_INVALID_ARG),
@@ -73,11 +76,18 @@ def test_other_entry_points_validate():
     assert lib.sol_attn_pool_blocks(*FAKE[:3], None, None, None, 1, 1, 64, 64, 64, 64, 0, None) == sb.SOL_ERR_INVALID_ARG
     assert lib.sol_attn_pool_blocks(None, *FAKE[1:3], FAKE[3], None, None, 1, 1, 64, 64, 64, 64, 0, None) == sb.SOL_ERR_INVALID_ARG
     assert lib.sol_attn_pool_blocks(*FAKE[:3], FAKE[3], None, None, 1, 1, 64, 80, 64, 64, 0, None) == sb.SOL_ERR_UNSUPPORTED
-    assert lib.sol_attn_thresholds(FAKE[0], FAKE[1], FAKE[2], None, None, 1, 1, 4, 8, 9, 64, 0.0, None) == sb.SOL_ERR_INVALID_ARG
-    assert lib.sol_attn_thresholds(FAKE[0], FAKE[1], FAKE[2], None, None, 1, 1, 4, 8, 8, 64, math.nan, None) == sb.SOL_ERR_INVALID_ARG
+    assert lib.sol_attn_thresholds(FAKE[0], FAKE[1], FAKE[2], None, None, 1, 1, 4, 8, 9, 64, 0.0, 0, None) == sb.SOL_ERR_INVALID_ARG
+    assert lib.sol_attn_thresholds(FAKE[0], FAKE[1], FAKE[2], None, None, 1, 1, 4, 8, 8, 64, math.nan, 0, None) == sb.SOL_ERR_INVALID_ARG
+    assert lib.sol_attn_thresholds(FAKE[0], FAKE[1], FAKE[2], None, None, 1, 1, 4, 8, 8, 64, 0.0, 1, None) == sb.SOL_ERR_INVALID_ARG
     arr = (ctypes.c_float * 4)()
     assert lib.sol_attn_stats(ctypes.cast(arr, P), 2, 2) == sb.SOL_ERR_NO_DATA
     assert lib.sol_attn_stats(None, 2, 2) == sb.SOL_ERR_INVALID_ARG
+
+
+def test_workspace_bytes_accepts_the_threshold_flag():
+    ws = sb.workspace_bytes
+    assert ws(1, 2, 1000, 128, 128, 64, sb.SOL_SPARSE | sb.SOL_THRESHOLD_DIAGONAL) == ws(1, 2, 1000, 128, 128, 64, "sparse")
+    assert ws(1, 2, 1000, 128, 128, 64, sb.SOL_SPARSE | 0x400) == 0
 
 
 def test_workspace_bytes():

@@ -46,14 +46,14 @@ def small_inputs(name):
     return _cache[name]
 
 
-def run_gpu(dev, w, q, k, v, beta, mode, want_mask=True):
+def run_gpu(dev, w, q, k, v, beta, mode, want_mask=True, threshold_mode="exact"):
     qd, kd, vd = (t.to(dev) for t in (q, k, v))
     nkr = w.NK - w.text_tokens // 64
     mw = sb.mask_words(nkr)
     mask = torch.zeros((w.B, w.H, w.NQ, mw), dtype=torch.int32, device=dev) if want_mask else None
     counts = torch.full((w.B, w.H), -1, dtype=torch.int32, device=dev)
     out = sb.forward(qd, kd, vd, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens,
-                     counts=counts, mask_out=mask)
+                     counts=counts, mask_out=mask, threshold_mode=threshold_mode)
     torch.cuda.synchronize()
     gmask = None
     if want_mask and mode != "dense":
@@ -102,6 +102,44 @@ def test_thresholds_parity(dev, name, beta):
     scale = 1 / math.sqrt(w.d)
     s_hat = ora.proxy_scores(to_np(qbar), to_np(kbar), scale)
     mu_r, sd_r = ora.row_stats(s_hat)
+    np.testing.assert_allclose(to_np(mu), mu_r, atol=1e-5, rtol=1e-5)
+    np.testing.assert_allclose(to_np(sigma), sd_r, atol=1e-5, rtol=1e-5)
+    tau_r = ora.thresholds(mu_r, sd_r, beta)
+    if math.isinf(beta):
+        assert np.array_equal(to_np(tau), tau_r)
+    else:
+        np.testing.assert_allclose(to_np(tau), tau_r, atol=1e-5, rtol=1e-5)
+
+
+@pytest.mark.parametrize("name", ["bf16_d128_q128", "f32_d64_q64", "bf16_d64_q64_text", "bf16_d128_q64_text"])
+@pytest.mark.parametrize("mode", ["sparse", "sparse_no_correction"])
+def test_forward_parity_diagonal_threshold(dev, name, mode):
+    # Appendix, Eq. appendix_diagonal_threshold selected through SOL_THRESHOLD_DIAGONAL.
+    w, (q, k, v) = small_inputs(name)
+    beta = 0.8
+    print(f"[parity] {name} mode={mode} diagonal thresholds", flush=True)
+    out, gmask, counts = run_gpu(dev, w, q, k, v, beta, mode, threshold_mode="diagonal")
+    qn, kn, vn = to_np(q), to_np(k), to_np(v)
+    ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens,
+                      threshold_mode="diagonal")
+    flips = assert_mask_matches(gmask, ref["mask"], ref["s_hat"], ref["tau"])
+    if flips:
+        ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens, mask=gmask)
+    assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
+    assert_output_close(to_np(out), ref["out"], w.dtype, f"{name}/{mode}/diagonal")
+
+
+@pytest.mark.parametrize("name", ["bf16_d128_q128", "f32_d64_q64"])
+@pytest.mark.parametrize("beta", [0.8, -INF])
+def test_thresholds_parity_diagonal(dev, name, beta):
+    w, (q, k, v) = small_inputs(name)
+    qbar, kbar, _ = sb.pool_blocks(q.to(dev), k.to(dev), v.to(dev), w.block_q, 64)
+    tau, mu, sigma = sb.thresholds(qbar, kbar, beta, threshold_mode="diagonal")
+    torch.cuda.synchronize()
+    scale = 1 / math.sqrt(w.d)
+    qb, kb = to_np(qbar), to_np(kbar)
+    mu_r, _ = ora.row_stats(ora.proxy_scores(qb, kb, scale))
+    sd_r = ora.diagonal_sigma(qb, kb, scale)
     np.testing.assert_allclose(to_np(mu), mu_r, atol=1e-5, rtol=1e-5)
     np.testing.assert_allclose(to_np(sigma), sd_r, atol=1e-5, rtol=1e-5)
     tau_r = ora.thresholds(mu_r, sd_r, beta)
@@ -195,3 +233,20 @@ def test_full_size_sampled(dev, full, mode):
     got = out[[b for b, _ in heads], [h for _, h in heads]].float().cpu().numpy()[None].astype(np.float64)
     rows = np.concatenate([np.arange(i * w.block_q, min((i + 1) * w.block_q, w.N)) for i in qblocks])
     assert_output_close(got[:, :, rows], ref["out"][:, :, rows], w.dtype, f"{w.name}/{mode}")
+
+
+def test_full_size_diagonal_threshold_mask(dev, full):
+    # The diagonal estimator at its own calibrated cutoff (same target density): GPU mask
+    # against the oracle's diagonal routing on every pair (bit-exact outside the 1e-3
+    # band), and its agreement with the exact estimator's mask.
+    w, (q, k, v), _, r = full
+    beta = configs.beta_for(w, threshold_mode="diagonal")
+    _, gmask, counts = run_gpu(dev, w, q, k, v, beta, "sparse_no_correction", threshold_mode="diagonal")
+    rd = ora.routing(q.float().numpy(), k.float().numpy(), w.block_q, 64, beta, keep_tail_tokens=w.text_tokens,
+                     threshold_mode="diagonal")
+    flips = assert_mask_matches(gmask, rd["mask"], rd["s_hat"], rd["tau"])
+    agree = float((rd["mask"] == r["mask"]).mean())
+    print(f"[parity] {w.name} diagonal thresholds: kept {float(rd['mask'].mean()):.4f} (exact "
+          f"{float(r['mask'].mean()):.4f}), mask agreement with exact {agree:.4f}, {flips} in-band flips",
+          flush=True)
+    assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
