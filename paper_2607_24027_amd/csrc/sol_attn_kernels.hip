@@ -82,11 +82,11 @@ struct Elem<float> {
 // combined through LDS.  Only the block's valid rows are read.
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ __launch_bounds__(256) void pool_mean_kernel(const T* __restrict__ x, float* __restrict__ mean,
-                                                        int N, int D, int blk, int nb) {
+__device__ __forceinline__ void pool_mean_block(const T* __restrict__ x, float* __restrict__ mean, int N, int D,
+                                                int blk, int nb, int j, int bh) {
     constexpr int EPC = Elem<T>::kPerChunk;
     __shared__ float red[256 * EPC];
-    const int j = blockIdx.x, bh = blockIdx.y, t = threadIdx.x;
+    const int t = threadIdx.x;
     const int cpr = D / EPC;
     const int groups = 256 / cpr;
     const int cc = t % cpr, g = t / cpr;
@@ -112,6 +112,12 @@ __global__ __launch_bounds__(256) void pool_mean_kernel(const T* __restrict__ x,
         for (int gg = 0; gg < groups; ++gg) s += red[gg * D + c];
         mean[((size_t)bh * nb + j) * D + c] = s * inv;
     }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void pool_mean_kernel(const T* __restrict__ x, float* __restrict__ mean,
+                                                        int N, int D, int blk, int nb) {
+    pool_mean_block<T>(x, mean, N, D, blk, nb, blockIdx.x, blockIdx.y);
 }
 
 // ---------------------------------------------------------------------------
@@ -249,14 +255,14 @@ constexpr int kMomSplit = 16;
 #define SOL_INLINE __attribute__((always_inline))
 
 template <int D>
-__global__ __launch_bounds__(256) void moments_partial_kernel(const float* __restrict__ kbar, double* __restrict__ part,
-                                                              int NK, int NKr) {
+__device__ __forceinline__ void moments_partial_block(const float* __restrict__ kbar, double* __restrict__ part, int NK,
+                                                      int NKr, int sp, int bh) {
     constexpr int SLAB = 32;
     constexpr int TS = D + 4;                  // f32 row stride of the staged slab
     constexpr int RB = D / 16;                 // 16x16 thread grid, RB x RB entries each
     __shared__ float x[SLAB * TS];
     __shared__ float k0[D];
-    const int sp = blockIdx.x, bh = blockIdx.y, t = threadIdx.x;
+    const int t = threadIdx.x;
     const float* kb = kbar + (size_t)bh * NK * D;
     const int j0 = (int)((long long)NKr * sp / kMomSplit), j1 = (int)((long long)NKr * (sp + 1) / kMomSplit);
     for (int c = t; c < D; c += 256) k0[c] = kb[c];
@@ -294,6 +300,13 @@ __global__ __launch_bounds__(256) void moments_partial_kernel(const float* __res
         for (int v = 0; v < RB; ++v) out[(r0 + u) * D + c0 + v] = s2[u][v];
     if (t < D) out[D * D + t] = s1;
 }
+
+template <int D>
+__global__ __launch_bounds__(256) void moments_partial_kernel(const float* __restrict__ kbar, double* __restrict__ part,
+                                                              int NK, int NKr) {
+    moments_partial_block<D>(kbar, part, NK, NKr, blockIdx.x, blockIdx.y);
+}
+
 
 template <int D>
 __global__ __launch_bounds__(256) void moments_final_kernel(const float* __restrict__ kbar, const double* __restrict__ part,
@@ -1427,16 +1440,22 @@ hipError_t launch_pool_mean(const void* x, float* mean, int dtype, int BH, int N
 
 size_t moments_scratch_bytes(int BH, int d) { return (size_t)BH * kMomSplit * ((size_t)d * d + d) * sizeof(double); }
 
+hipError_t launch_moments_final(const float* kbar, float* muk, float* cov, double* scratch, int BH, int NK, int NKr,
+                                int d, hipStream_t st) {
+    if (d == 128)
+        moments_final_kernel<128><<<dim3(128 * 128 / 256, BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr);
+    else
+        moments_final_kernel<64><<<dim3(64 * 64 / 256, BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr);
+    return hipGetLastError();
+}
+
 hipError_t launch_moments(const float* kbar, float* muk, float* cov, double* scratch, int BH, int NK, int NKr, int d,
                           hipStream_t st) {
-    if (d == 128) {
-        moments_partial_kernel<128><<<dim3(kMomSplit, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr);
-        moments_final_kernel<128><<<dim3(128 * 128 / 256, BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr);
-    } else {
-        moments_partial_kernel<64><<<dim3(kMomSplit, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr);
-        moments_final_kernel<64><<<dim3(64 * 64 / 256, BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr);
-    }
-    return hipGetLastError();
+    if (d == 128) moments_partial_kernel<128><<<dim3(kMomSplit, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr);
+    else moments_partial_kernel<64><<<dim3(kMomSplit, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_moments_final(kbar, muk, cov, scratch, BH, NK, NKr, d, st);
 }
 
 hipError_t launch_tau(const float* qbar, const float* muk, const float* cov, float* tau, float* mu, float* sigma,
@@ -1461,10 +1480,6 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
     hipError_t e;
     const float scale = 1.0f / sqrtf((float)d);
     if (s.dtype == kBF16) {
-        if (routing) {
-            e = launch_pool_mean(q, ws.qbar, kBF16, s.BH, s.N, d, s.bq, st);
-            if (e != hipSuccess) return e;
-        }
         const int nj = routing ? (s.NC * kChunk > s.NK ? s.NC * kChunk : s.NK) : s.NK;
         const uint16_t* kk = static_cast<const uint16_t*>(k);
         const uint16_t* vv = static_cast<const uint16_t*>(v);
@@ -1476,6 +1491,7 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
                                                                      s.NK, s.NKr, s.NC, routing ? 1 : 0);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (routing) {
+            if ((e = launch_pool_mean(q, ws.qbar, kBF16, s.BH, s.N, d, s.bq, st)) != hipSuccess) return e;
             if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, ws.mom, s.BH, s.NK, s.NKr, d, st)) != hipSuccess) return e;
             if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, s.diag, st)) != hipSuccess)
                 return e;

@@ -92,6 +92,46 @@ def test_pool_blocks_parity(dev, name):
         np.testing.assert_allclose(to_np(got), want, rtol=1e-5, atol=2e-6)
 
 
+def test_pool_blocks_long_blocks(dev):
+    # The pooling entry point takes any block size; blocks longer than 128 rows take the
+    # row-by-row tail path.
+    w, (q, k, v) = small_inputs("bf16_d128_q128")
+    for blk in (200, 1000):
+        qbar, _, _ = sb.pool_blocks(q.to(dev), k.to(dev), v.to(dev), blk, 64)
+        torch.cuda.synchronize()
+        want, _ = ora.pool_means(to_np(q), blk)
+        np.testing.assert_allclose(to_np(qbar), want, rtol=1e-5, atol=2e-6)
+
+
+EDGE = {
+    # name: (grid, d, block_q, dtype, text tokens, B, H)
+    "n1": ((1, 1), 128, 128, "bf16", 0, 1, 1),            # one token: one query and one key block
+    "n63": ((7, 9), 64, 64, "bf16", 0, 1, 2),             # one ragged block of each kind
+    "n65": ((5, 13), 128, 128, "bf16", 0, 2, 3),          # B=2, H=3; a 1-token last key block
+    "one_routable": ((1, 64), 128, 64, "bf16", 64, 1, 2), # N=128 with 64 text tokens: one routable block
+    "f32_n100": ((10, 10), 64, 128, "f32", 0, 2, 1),      # f32 path, ragged, B=2
+}
+
+
+@pytest.mark.parametrize("name", list(EDGE))
+@pytest.mark.parametrize("mode,beta", [("dense", 0.0), ("sparse", 0.5), ("sparse", -INF),
+                                       ("sparse_no_correction", 0.5), ("sparse_no_correction", -0.3)])
+def test_forward_parity_edge_shapes(dev, name, mode, beta):
+    grid, d, bq, dtype, text, B, H = EDGE[name]
+    w = small_workload(name, grid, d, bq, dtype=dtype, text_tokens=text, H=H, B=B, seed=23)
+    q, k, v = synth.make_qkv(w)
+    print(f"[parity] edge {name} N={w.N} mode={mode} beta={beta}", flush=True)
+    out, gmask, counts = run_gpu(dev, w, q, k, v, beta, mode)
+    qn, kn, vn = to_np(q), to_np(k), to_np(v)
+    ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens)
+    if mode != "dense":
+        flips = assert_mask_matches(gmask, ref["mask"], ref["s_hat"], ref["tau"])
+        if flips:
+            ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens, mask=gmask)
+        assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
+    assert_output_close(to_np(out), ref["out"], w.dtype, f"edge {name}/{mode}/{beta}")
+
+
 @pytest.mark.parametrize("name", ["bf16_d128_q128", "f32_d64_q64"])
 @pytest.mark.parametrize("beta", [0.8, -0.5, -INF, INF])
 def test_thresholds_parity(dev, name, beta):
