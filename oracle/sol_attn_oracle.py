@@ -122,6 +122,31 @@ def route(s_hat: np.ndarray, tau: np.ndarray) -> np.ndarray:
     return s_hat > tau[..., None]
 
 
+def route_topk(s_hat: np.ndarray, k: int) -> np.ndarray:
+    """Top-k routing, the fixed-budget baseline of Section 2: the k largest proxies of
+    each row (ties go to the lower key-block index)."""
+    order = np.argsort(-s_hat, axis=-1, kind="stable")
+    mask = np.zeros(s_hat.shape, dtype=bool)
+    np.put_along_axis(mask, order[..., :min(k, s_hat.shape[-1])], True, axis=-1)
+    return mask
+
+
+def route_topp(s_hat: np.ndarray, p: float) -> np.ndarray:
+    """Top-p routing, the cumulative-mass baseline of Section 2: over the block softmax
+    p_hat_i = Softmax(s_hat_i) (Eq. block_proxy), the shortest prefix of blocks in
+    decreasing proxy order (ties to the lower index) whose mass reaches p; a block is kept
+    when the mass of the blocks before it is below p."""
+    order = np.argsort(-s_hat, axis=-1, kind="stable")
+    srt = np.take_along_axis(s_hat, order, axis=-1)
+    w = np.exp(srt - srt[..., :1])
+    mass = w / w.sum(axis=-1, keepdims=True)
+    before = np.cumsum(mass, axis=-1) - mass
+    keep_sorted = before < p
+    mask = np.zeros(s_hat.shape, dtype=bool)
+    np.put_along_axis(mask, order, keep_sorted, axis=-1)
+    return mask
+
+
 # ---------------------------------------------------------------------------
 # Combined softmax terms (Section 3.2, Eqs. solattn_denominator / numerator)
 # ---------------------------------------------------------------------------

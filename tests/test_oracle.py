@@ -119,6 +119,29 @@ def test_chunked_thresholding_recovers_full_row_set():
         assert np.array_equal(sel, r["mask"])
 
 
+def test_topk_and_topp_brute_force():
+    # The routing baselines written out by hand on tiny rows: top-k keeps the k largest
+    # (ties to the lower index); top-p keeps blocks while the softmax mass before them
+    # (in decreasing order) is below p.
+    rows = np.array([[0.5, 2.0, -1.0, 2.0, 0.3],
+                     [1.0, 1.0, 1.0, 1.0, 1.0],
+                     [3.0, 0.0, 0.0, -2.0, 1.0]])
+    assert ora.route_topk(rows, 2).tolist() == [[False, True, False, True, False],
+                                                  [True, True, False, False, False],
+                                                  [True, False, False, False, True]]
+    for p in (0.05, 0.3, 0.5, 0.9, 0.999, 1.0):
+        got = ora.route_topp(rows, p)
+        for r, row in enumerate(rows):
+            order = sorted(range(len(row)), key=lambda j: (-row[j], j))
+            z = sum(math.exp(x) for x in row)
+            acc, want = 0.0, [False] * len(row)
+            for j in order:
+                if acc < p:
+                    want[j] = True
+                acc += math.exp(row[j]) / z
+            assert got[r].tolist() == want, (p, r)
+
+
 def hadamard(n):
     h = np.array([[1.0]])
     while h.shape[0] < n:
