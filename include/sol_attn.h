@@ -98,6 +98,30 @@ int sol_attn_thresholds(const float* qbar, const float* kbar,
                         float beta, int threshold_mode, void* stream);
 
 /*
+ * Baseline routing with a materialised proxy map (Section 2, after Eq. block_proxy:
+ * "standard routing applies top-k to s_hat_i or top-p to p_hat_i"), provided to measure
+ * what the on-the-fly threshold routing of the forward calls avoids; the forward never
+ * uses it.
+ *
+ * Writes proxies[b,h,i,j] = s * Qbar_i . Kbar_j (s = 1/sqrt(d)) for the first nk_routable
+ * key blocks, then selects per query block:
+ *   SOL_ROUTE_TOPK: the param = k largest proxies (1 <= k <= nk_routable, nk_routable <= 8192);
+ *   SOL_ROUTE_TOPP: the shortest prefix of the blocks in decreasing proxy order whose mass
+ *     under p_hat_i = Softmax(s_hat_i) reaches param = p (0 < p <= 1; a block is kept while
+ *     the mass before it is below p; nk_routable <= 4096).
+ * Ties go to the lower key-block index.
+ *
+ * qbar: [B,H,NQ,d] f32 device; kbar: [B,H,NK,d] f32 device (NK >= nk_routable);
+ * proxies: [B,H,NQ,nk_routable] f32 device (written; caller-owned scratch);
+ * mask_out: [B,H,NQ,ceil(nk_routable/32)] u32 device bit mask (bit j%32 of word j/32).
+ * Asynchronous on `stream`.
+ */
+enum { SOL_ROUTE_TOPK = 0, SOL_ROUTE_TOPP = 1 };
+int sol_attn_route_materialized(const float* qbar, const float* kbar, float* proxies, uint32_t* mask_out,
+                                int B, int H, int NQ, int NK, int nk_routable, int d,
+                                int rule, float param, void* stream);
+
+/*
  * Routed attention forward, short form: bf16 q/k/v/out, default stream,
  * library-managed workspace, per-head counts kept for sol_attn_stats().
  * `tau` is the standardised cutoff beta of Eq. threshold_routing; mode is one

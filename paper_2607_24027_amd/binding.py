@@ -33,6 +33,7 @@ SIGNATURES = {
     "sol_attn_stats": (_I, [_P, _I, _I]),
     "sol_attn_timing_enable": (_I, [_I]),
     "sol_attn_kernel_timing": (_I, [_P, _P]),
+    "sol_attn_route_materialized": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P]),
     "sol_attn_last_error": (ctypes.c_char_p, []),
     "sol_attn_release": (_I, []),
 }
@@ -128,6 +129,28 @@ def thresholds(qbar, kbar, beta: float, nk_routable: Optional[int] = None, thres
 
 def _mode_code(mode, threshold_mode="exact") -> int:
     return (MODES[mode] if isinstance(mode, str) else int(mode)) | THRESHOLD_MODES[threshold_mode]
+
+
+SOL_ROUTE_TOPK, SOL_ROUTE_TOPP = 0, 1
+
+
+def route_materialized(qbar, kbar, rule: str, param: float, nk_routable: Optional[int] = None, proxies=None,
+                       mask_out=None):
+    """Baseline routing through a materialised proxy map: rule "topk" (param = k) or "topp"
+    (param = p).  Returns (proxies [B,H,NQ,NKr] f32, mask [B,H,NQ,MW] int32) device tensors."""
+    import torch
+    B, H, NQ, d = qbar.shape
+    NK = kbar.shape[2]
+    nkr = NK if nk_routable is None else nk_routable
+    if proxies is None:
+        proxies = torch.empty((B, H, NQ, nkr), device=qbar.device, dtype=torch.float32)
+    if mask_out is None:
+        mask_out = torch.empty((B, H, NQ, mask_words(nkr)), device=qbar.device, dtype=torch.int32)
+    code = {"topk": SOL_ROUTE_TOPK, "topp": SOL_ROUTE_TOPP}[rule]
+    _check(lib().sol_attn_route_materialized(_ptr(qbar.contiguous()), _ptr(kbar.contiguous()), _ptr(proxies),
+                                             _ptr(mask_out), B, H, NQ, NK, nkr, d, code, float(param),
+                                             _stream(qbar.device)))
+    return proxies, mask_out
 
 
 def workspace_bytes(B, H, N, d, block_q, block_k, mode, dtype=SOL_BF16, keep_tail_tokens=0) -> int:

@@ -152,6 +152,31 @@ int sol_attn_thresholds(const float* qbar, const float* kbar, float* tau, float*
     return ok();
 }
 
+int sol_attn_route_materialized(const float* qbar, const float* kbar, float* proxies, uint32_t* mask_out, int B, int H,
+                                int NQ, int NK, int nk_routable, int d, int rule, float param, void* stream) {
+    if (!qbar || !kbar || !proxies || !mask_out)
+        return fail(SOL_ERR_INVALID_ARG, "qbar, kbar, proxies and mask_out must be non-null");
+    if (B <= 0 || H <= 0 || NQ <= 0 || NK <= 0) return fail(SOL_ERR_INVALID_ARG, "B, H, NQ and NK must be positive");
+    if (nk_routable <= 0 || nk_routable > NK) return fail(SOL_ERR_INVALID_ARG, "nk_routable must be in [1, NK]");
+    if (d != 64 && d != 128) return fail(SOL_ERR_UNSUPPORTED, "d must be 64 or 128 (got %d)", d);
+    if ((long long)B * H > (1LL << 24) || (long long)NQ > (1 << 20))
+        return fail(SOL_ERR_UNSUPPORTED, "too many (b, h) pairs or query blocks");
+    if (rule == SOL_ROUTE_TOPK) {
+        if (!(param >= 1.f && param <= (float)nk_routable) || param != std::floor(param))
+            return fail(SOL_ERR_INVALID_ARG, "top-k needs an integer k in [1, nk_routable] (got %g)", (double)param);
+        if (nk_routable > 8192) return fail(SOL_ERR_UNSUPPORTED, "top-k supports at most 8192 key blocks");
+    } else if (rule == SOL_ROUTE_TOPP) {
+        if (!(param > 0.f && param <= 1.f)) return fail(SOL_ERR_INVALID_ARG, "top-p needs p in (0, 1] (got %g)", (double)param);
+        if (nk_routable > 4096) return fail(SOL_ERR_UNSUPPORTED, "top-p supports at most 4096 key blocks");
+    } else {
+        return fail(SOL_ERR_INVALID_ARG, "rule must be SOL_ROUTE_TOPK or SOL_ROUTE_TOPP (got %d)", rule);
+    }
+    hipError_t e = sol::launch_route_materialized(qbar, kbar, proxies, mask_out, B * H, NQ, NK, nk_routable, d, rule,
+                                                  param, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "materialised routing");
+    return ok();
+}
+
 size_t sol_attn_workspace_bytes(int B, int H, int N, int d, int block_q, int block_k, int mode, int dtype,
                                 int keep_tail_tokens) {
     static const char dummy = 0;

@@ -58,6 +58,9 @@ hipError_t launch_moments(const float* kbar, float* muk, float* cov, double* scr
                           int d, hipStream_t st);
 hipError_t launch_tau(const float* qbar, const float* muk, const float* cov, float* tau, float* mu,
                       float* sigma, int BH, int NQ, int d, float beta, int diag, hipStream_t st);
+// Materialised-proxy routing baselines (top-k: rule 0, param = k; top-p: rule 1, param = p).
+hipError_t launch_route_materialized(const float* qbar, const float* kbar, float* shat, uint32_t* mask, int BH, int NQ,
+                                     int NK, int NKr, int d, int rule, float param, hipStream_t st);
 // ev_start/ev_stop (nullable) are recorded on `st` around the fused attention kernel.
 hipError_t launch_forward(const Shape& s, const void* q, const void* k, const void* v, void* out,
                           float beta, const Workspace& ws, uint32_t* counts, uint32_t* mask_out,

@@ -23,7 +23,7 @@ def header_functions():
 def test_library_exports_every_declared_symbol():
     lib = sb.lib()
     names = header_functions()
-    assert len(names) == 10
+    assert len(names) == 11
     for name in names:
         assert hasattr(lib, name), name
     assert set(names) == set(sb.SIGNATURES)
@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 def test_header_constants_match_binding():
     text = open(HEADER).read()
     for name, val in [("SOL_DENSE", 0), ("SOL_SPARSE", 1), ("SOL_SPARSE_NO_CORRECTION", 2), ("SOL_BF16", 0),
-                      ("SOL_THRESHOLD_DIAGONAL", 0x100),
+                      ("SOL_THRESHOLD_DIAGONAL", 0x100), ("SOL_ROUTE_TOPK", 0), ("SOL_ROUTE_TOPP", 1),
                       ("SOL_F32", 1), ("SOL_ERR_INVALID_ARG", -1), ("SOL_ERR_UNSUPPORTED", -2),
                       ("SOL_ERR_HIP", -3), ("SOL_ERR_WORKSPACE", -4), ("SOL_ERR_NO_DATA", -5)]:
         m = re.search(rf"\b{name}\s*=\s*(-?(?:0x[0-9a-fA-F]+|\d+))", text)
@@ -79,6 +79,14 @@ def test_other_entry_points_validate():
     assert lib.sol_attn_thresholds(FAKE[0], FAKE[1], FAKE[2], None, None, 1, 1, 4, 8, 9, 64, 0.0, 0, None) == sb.SOL_ERR_INVALID_ARG
     assert lib.sol_attn_thresholds(FAKE[0], FAKE[1], FAKE[2], None, None, 1, 1, 4, 8, 8, 64, math.nan, 0, None) == sb.SOL_ERR_INVALID_ARG
     assert lib.sol_attn_thresholds(FAKE[0], FAKE[1], FAKE[2], None, None, 1, 1, 4, 8, 8, 64, 0.0, 1, None) == sb.SOL_ERR_INVALID_ARG
+    rm = lib.sol_attn_route_materialized
+    assert rm(FAKE[0], FAKE[1], FAKE[2], None, 1, 1, 4, 8, 8, 64, 0, 2.0, None) == sb.SOL_ERR_INVALID_ARG
+    assert rm(FAKE[0], FAKE[1], FAKE[2], FAKE[3], 1, 1, 4, 8, 8, 64, 0, 9.0, None) == sb.SOL_ERR_INVALID_ARG
+    assert rm(FAKE[0], FAKE[1], FAKE[2], FAKE[3], 1, 1, 4, 8, 8, 64, 0, 2.5, None) == sb.SOL_ERR_INVALID_ARG
+    assert rm(FAKE[0], FAKE[1], FAKE[2], FAKE[3], 1, 1, 4, 8, 8, 64, 1, 0.0, None) == sb.SOL_ERR_INVALID_ARG
+    assert rm(FAKE[0], FAKE[1], FAKE[2], FAKE[3], 1, 1, 4, 8, 8, 64, 2, 0.5, None) == sb.SOL_ERR_INVALID_ARG
+    assert rm(FAKE[0], FAKE[1], FAKE[2], FAKE[3], 1, 1, 4, 5000, 5000, 64, 1, 0.5, None) == sb.SOL_ERR_UNSUPPORTED
+    assert rm(FAKE[0], FAKE[1], FAKE[2], FAKE[3], 1, 1, 4, 8, 8, 80, 0, 2.0, None) == sb.SOL_ERR_UNSUPPORTED
     arr = (ctypes.c_float * 4)()
     assert lib.sol_attn_stats(ctypes.cast(arr, P), 2, 2) == sb.SOL_ERR_NO_DATA
     assert lib.sol_attn_stats(None, 2, 2) == sb.SOL_ERR_INVALID_ARG

@@ -290,3 +290,52 @@ def test_full_size_diagonal_threshold_mask(dev, full):
           f"{float(r['mask'].mean()):.4f}), mask agreement with exact {agree:.4f}, {flips} in-band flips",
           flush=True)
     assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
+
+
+# --------------------------------------------------------------------------- routing baselines
+
+def check_baseline_masks(gmask, ref_mask, s_hat, rule):
+    """GPU top-k / top-p mask against the oracle's on the same proxies: differences only at
+    near-ties of the cut (proxies within 1e-3 of the smallest kept one)."""
+    diff = gmask != ref_mask
+    if rule == "topk":
+        assert np.array_equal(gmask.sum(-1), ref_mask.sum(-1))
+    else:
+        assert np.all(np.abs(gmask.sum(-1).astype(np.int64) - ref_mask.sum(-1)) <= 2)
+    cut = np.where(ref_mask, s_hat, np.inf).min(axis=-1, keepdims=True)
+    near = np.abs(s_hat - cut) < 1e-3
+    assert not (diff & ~near).any(), f"{int((diff & ~near).sum())} baseline mask differences away from the cut"
+    return int(diff.sum())
+
+
+@pytest.mark.parametrize("name", ["bf16_d128_q128", "f32_d64_q64", "bf16_d64_q64_text"])
+@pytest.mark.parametrize("rule,param", [("topk", 1), ("topk", 7), ("topk", 25), ("topp", 0.05), ("topp", 0.5),
+                                        ("topp", 0.95), ("topp", 1.0)])
+def test_route_materialized_small(dev, name, rule, param):
+    w, (q, k, v) = small_inputs(name)
+    nkr = w.NK - w.text_tokens // 64
+    if rule == "topk" and param > nkr:
+        pytest.skip("k larger than the routable blocks")
+    qbar, kbar, _ = sb.pool_blocks(q.to(dev), k.to(dev), v.to(dev), w.block_q, 64)
+    prox, mask = sb.route_materialized(qbar, kbar, rule, param, nk_routable=nkr)
+    torch.cuda.synchronize()
+    s_hat = ora.proxy_scores(to_np(qbar), to_np(kbar)[:, :, :nkr], 1 / math.sqrt(w.d))
+    np.testing.assert_allclose(to_np(prox), s_hat, atol=1e-5, rtol=1e-5)
+    gmask = sb.unpack_mask(mask.cpu().numpy().view(np.uint32), nkr)
+    ref = ora.route_topk(s_hat, param) if rule == "topk" else ora.route_topp(s_hat, param)
+    check_baseline_masks(gmask, ref, s_hat, rule)
+
+
+def test_route_materialized_full_720p(dev):
+    w = configs.WORKLOADS["video720p"]
+    q, k, v = synth.make_qkv(w, heads=[(0, 0), (0, 1)], workers=synth.default_workers())
+    q, k, v = q[:, :2].contiguous(), k[:, :2].contiguous(), v[:, :2].contiguous()
+    qbar, kbar, _ = sb.pool_blocks(q.to(dev), k.to(dev), v.to(dev), w.block_q, 64)
+    s_hat = ora.proxy_scores(to_np(qbar), to_np(kbar), 1 / math.sqrt(w.d))
+    for rule, param in (("topk", 177), ("topp", 0.32)):
+        _, mask = sb.route_materialized(qbar, kbar, rule, param)
+        torch.cuda.synchronize()
+        gmask = sb.unpack_mask(mask.cpu().numpy().view(np.uint32), w.NK)
+        ref = ora.route_topk(s_hat, param) if rule == "topk" else ora.route_topp(s_hat, param)
+        n = check_baseline_masks(gmask, ref, s_hat, rule)
+        print(f"[parity] 720p {rule}({param}): {n} near-cut differences, kept {gmask.mean():.4f}", flush=True)
