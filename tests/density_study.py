@@ -8,8 +8,8 @@ from one block up to ceil(pN)).  On the synthetic workloads this script reports:
   * the mean kept fraction of threshold routing against rho_G(beta) over a range of beta;
   * at a common mean density (15 %), the distribution of per-query-block densities
     (p10 / p25 / median / p75 / p90) for threshold routing (beta calibrated), top-k
-    (k = round(0.15 * NK_routable)) and top-p (p calibrated; mass = softmax of the
-    scaled proxies s_hat_i with the block multiplicities n_j).
+    (k = round(0.15 * NK_routable)) and top-p (p calibrated; mass = Softmax(s_hat_i) as in
+    Eq. block_proxy), both through the oracle's route_topk / route_topp.
 
     python tests/density_study.py [workload ...]
 """
@@ -55,7 +55,6 @@ def main():
                         keep_tail_tokens=w.text_tokens)
         s_hat, mu, sigma = r["s_hat"], r["mu"], r["sigma"]        # [B,H,NQ,NKr]
         nkr = s_hat.shape[-1]
-        counts = ora.block_counts(w.N, w.block_k)[:nkr].astype(np.float64)
 
         def kept(beta):
             return float(ora.route(s_hat, ora.thresholds(mu, sigma, beta)).mean())
@@ -68,19 +67,20 @@ def main():
         dens_thr = ora.route(s_hat, ora.thresholds(mu, sigma, beta)).mean(axis=-1).ravel()
         # top-k: a fixed count per query block
         kk = int(round(TARGET * nkr))
-        dens_topk = np.full(dens_thr.shape, kk / nkr)
-        # top-p: smallest prefix (descending proxies) holding mass p of softmax(s_hat + log n_j)
-        logits = s_hat + np.log(counts)
-        order = np.argsort(-logits, axis=-1)
-        srt = np.take_along_axis(logits, order, axis=-1)
+        dens_topk = ora.route_topk(s_hat, kk).mean(axis=-1).ravel()
+        # top-p: p is calibrated on the sorted cumulative mass (computed once), then the
+        # densities are taken from the oracle's route_topp at that p
+        order = np.argsort(-s_hat, axis=-1, kind="stable")
+        srt = np.take_along_axis(s_hat, order, axis=-1)
         prob = np.exp(srt - srt[..., :1])
-        cum = np.cumsum(prob, axis=-1) / prob.sum(axis=-1, keepdims=True)
+        prob /= prob.sum(axis=-1, keepdims=True)
+        before = np.cumsum(prob, axis=-1) - prob
 
         def topp_counts(p):
-            return (cum < p).sum(axis=-1) + 1      # include the block that crosses p
+            return (before < p).sum(axis=-1)
 
         p = bisect(lambda pp: -float(topp_counts(pp).mean() / nkr), 0.0, 1.0, -TARGET)
-        dens_topp = (topp_counts(p) / nkr).ravel()
+        dens_topp = ora.route_topp(s_hat, p).mean(axis=-1).ravel()
         rec = {"workload": name, "nk_routable": nkr, "gaussian_reference": gauss,
                "common_density": TARGET,
                "threshold": {"beta": beta, "mean": float(dens_thr.mean()), **pcts(dens_thr)},
