@@ -31,7 +31,15 @@ notes of the repository):
   * ``keep_tail_tokens`` trailing tokens (text tokens of an MMDiT; Appendix,
     "Generation Configurations") form forced key blocks that are always computed
     exactly and take no part in routing statistics;
-  * a row with no term at all (only possible without the correction) outputs 0.
+  * a row with no term at all (only possible without the correction) outputs 0;
+  * causal masks (an extension the Appendix names as future work: row-dependent masks
+    need centring and multiplicity over valid keys).  With granule G, key s is visible
+    to query t iff s < min((t // G + 1) G, N): G = 1 is token-causal attention, G = a
+    frame's token count is frame-causal attention.  Key blocks visible to every row of
+    a query block are its routable blocks: mu_i and sigma_i are taken over them only and
+    their multiplicity is their full valid-token count.  Key blocks visible to some rows
+    only are computed exactly under the token mask, like forced blocks; blocks visible
+    to none are skipped.
 """
 from __future__ import annotations
 
@@ -122,6 +130,54 @@ def route(s_hat: np.ndarray, tau: np.ndarray) -> np.ndarray:
     return s_hat > tau[..., None]
 
 
+# ---------------------------------------------------------------------------
+# Causal masks (extension: the Appendix's row-dependent masks)
+# ---------------------------------------------------------------------------
+
+def causal_limits(n_tokens: int, granule: int) -> np.ndarray:
+    """lim[t] = min((t // G + 1) * G, N): query t sees exactly the keys s < lim[t]."""
+    t = np.arange(n_tokens, dtype=np.int64)
+    return np.minimum((t // granule + 1) * granule, n_tokens)
+
+
+def causal_block_ranges(n_tokens: int, block_q: int, block_k: int, granule: int):
+    """Per query block i, (r_i, e_i): key blocks [0, r_i) are visible to every row of
+    the block (its routable blocks), [r_i, e_i) to some rows only, [e_i, NK) to none.
+    Visibility is a prefix of the keys and lim[t] grows with t, so the first row of a
+    block fixes r_i and its last row fixes e_i."""
+    lim = causal_limits(n_tokens, granule)
+    kcounts = block_counts(n_tokens, block_k)
+    kend = np.arange(len(kcounts)) * block_k + kcounts          # exclusive end of each key block
+    kstart = np.arange(len(kcounts)) * block_k
+    nq = -(-n_tokens // block_q)
+    r = np.empty(nq, dtype=np.int64)
+    e = np.empty(nq, dtype=np.int64)
+    for i in range(nq):
+        lo = lim[i * block_q]
+        hi = lim[min((i + 1) * block_q, n_tokens) - 1]
+        r[i] = int(np.count_nonzero(kend <= lo))
+        e[i] = int(np.count_nonzero(kstart < hi))
+    return r, e
+
+
+def causal_row_stats(s_hat: np.ndarray, r: np.ndarray):
+    """mu_i and sigma_i over the routable prefix j < r_i of each proxy row (population
+    normaliser 1/r_i, as for the full row); NaN where r_i = 0."""
+    valid = np.arange(s_hat.shape[-1])[None, :] < r[:, None]
+    cnt = np.where(r > 0, r, 1).astype(np.float64)
+    mu = np.where(valid, s_hat, 0.0).sum(axis=-1) / cnt
+    var = np.where(valid, (s_hat - mu[..., None]) ** 2, 0.0).sum(axis=-1) / cnt
+    mu = np.where(r > 0, mu, np.nan)
+    return mu, np.where(r > 0, np.sqrt(var), np.nan)
+
+
+def causal_route(s_hat: np.ndarray, tau: np.ndarray, r: np.ndarray) -> np.ndarray:
+    """S_i = {j < r_i : s_hat_ij > tau_i}."""
+    valid = np.arange(s_hat.shape[-1])[None, :] < r[:, None]
+    with np.errstate(invalid="ignore"):
+        return valid & (s_hat > tau[..., None])
+
+
 def route_topk(s_hat: np.ndarray, k: int) -> np.ndarray:
     """Top-k routing, the fixed-budget baseline of Section 2: the k largest proxies of
     each row (ties go to the lower key-block index)."""
@@ -151,10 +207,13 @@ def route_topp(s_hat: np.ndarray, p: float) -> np.ndarray:
 # Combined softmax terms (Section 3.2, Eqs. solattn_denominator / numerator)
 # ---------------------------------------------------------------------------
 
-def exact_terms(q_rows, keys, values, scale, shift):
+def exact_terms(q_rows, keys, values, scale, shift, visible=None):
     """Exact-branch contributions of a set of keys to each row:
-    D = sum_u exp(scale q.k_u - shift),  N = sum_u exp(scale q.k_u - shift) v_u."""
+    D = sum_u exp(scale q.k_u - shift),  N = sum_u exp(scale q.k_u - shift) v_u,
+    the sums running over the keys a row sees (``visible`` [rows, keys], causal masks)."""
     w = np.exp(scale * (q_rows @ keys.T) - shift[:, None])
+    if visible is not None:
+        w = np.where(visible, w, 0.0)
     return w.sum(axis=1), w @ values
 
 
@@ -167,7 +226,7 @@ def approx_terms(q_rows, kbar_blocks, vhat_blocks, counts, scale, shift):
 
 
 def _forward_head(args):
-    (qh, kh, vh, block_q, block_k, beta, mode, n_forced, qblocks, mask_h, threshold_mode) = args
+    (qh, kh, vh, block_q, block_k, beta, mode, n_forced, qblocks, mask_h, threshold_mode, granule) = args
     qh = np.asarray(qh, dtype=np.float64)
     kh = np.asarray(kh, dtype=np.float64)
     vh = np.asarray(vh, dtype=np.float64)
@@ -180,54 +239,74 @@ def _forward_head(args):
     vhat = np.stack([vh[j * block_k: j * block_k + c].sum(axis=0) for j, c in enumerate(kcounts)])
 
     s_hat = proxy_scores(qbar, kbar[:nkr], scale)
-    mu, sigma = row_stats(s_hat)
-    if threshold_mode == "diagonal":
-        sigma = diagonal_sigma(qbar, kbar[:nkr], scale)
+    if granule:
+        lim = causal_limits(n, granule)
+        r_blk, e_blk = causal_block_ranges(n, block_q, block_k, granule)
+        mu, sigma = causal_row_stats(s_hat, r_blk)
+    else:
+        r_blk = np.full(len(qbar), nkr, dtype=np.int64)
+        e_blk = np.full(len(qbar), nk, dtype=np.int64)
+        mu, sigma = row_stats(s_hat)
+        if threshold_mode == "diagonal":
+            sigma = diagonal_sigma(qbar, kbar[:nkr], scale)
     tau = thresholds(mu, sigma, beta)
-    sel = route(s_hat, tau) if mask_h is None else np.asarray(mask_h, dtype=bool)
-    band = int(np.count_nonzero(np.abs(s_hat - tau[:, None]) < BAND))
+    if mask_h is not None:
+        sel = np.asarray(mask_h, dtype=bool)
+    else:
+        sel = causal_route(s_hat, tau, r_blk) if granule else route(s_hat, tau)
+    routable = np.arange(nkr)[None, :] < r_blk[:, None]
+    with np.errstate(invalid="ignore"):
+        band = int(np.count_nonzero(routable & (np.abs(s_hat - tau[:, None]) < BAND)))
 
     out = np.full((n, d), np.nan)
-    forced = list(range(nkr, nk))
     for i in qblocks:
         r0, r1 = i * block_q, min((i + 1) * block_q, n)
         q_rows = qh[r0:r1]
+        ri, ei = int(r_blk[i]), int(e_blk[i])
+        forced = list(range(ri, ei)) if granule else list(range(nkr, nk))
         if mode == "dense":
-            exact_blocks, approx_blocks = list(range(nk)), []
+            exact_blocks, approx_blocks = list(range(ei)), []
         else:
-            exact_blocks = [j for j in range(nkr) if sel[i, j]] + forced
-            approx_blocks = [j for j in range(nkr) if not sel[i, j]] if mode == "sparse" else []
+            exact_blocks = [j for j in range(ri) if sel[i, j]] + forced
+            approx_blocks = [j for j in range(ri) if not sel[i, j]] if mode == "sparse" else []
         key_idx = np.concatenate([np.arange(j * block_k, j * block_k + kcounts[j]) for j in exact_blocks]) \
             if exact_blocks else np.zeros(0, dtype=np.int64)
+        visible = key_idx[None, :] < lim[r0:r1, None] if granule else None
         ab = np.asarray(approx_blocks, dtype=np.int64)
         # Row shift for overflow safety: the largest exponent of any term.
         cand = []
         if key_idx.size:
-            cand.append((scale * (q_rows @ kh[key_idx].T)).max(axis=1))
+            lg = scale * (q_rows @ kh[key_idx].T)
+            if visible is not None:
+                lg = np.where(visible, lg, -np.inf)
+            cand.append(lg.max(axis=1))
         if ab.size:
             cand.append((scale * (q_rows @ kbar[ab].T) + np.log(kcounts[ab])).max(axis=1))
         if not cand:
             out[r0:r1] = 0.0
             continue
         shift = np.max(np.stack(cand), axis=0)
+        empty = ~np.isfinite(shift)        # causal rows with no visible term (no correction)
+        shift = np.where(empty, 0.0, shift)
         den = np.zeros(r1 - r0)
         num = np.zeros((r1 - r0, d))
         if key_idx.size:
-            dd, nn = exact_terms(q_rows, kh[key_idx], vh[key_idx], scale, shift)
+            dd, nn = exact_terms(q_rows, kh[key_idx], vh[key_idx], scale, shift, visible)
             den += dd
             num += nn
         if ab.size:
             dd, nn = approx_terms(q_rows, kbar[ab], vhat[ab], kcounts[ab], scale, shift)
             den += dd
             num += nn
-        out[r0:r1] = num / den[:, None]
-    return out, sel, s_hat, tau, mu, sigma, band
+        with np.errstate(invalid="ignore", divide="ignore"):
+            out[r0:r1] = np.where(den[:, None] > 0, num / np.where(den > 0, den, 1.0)[:, None], 0.0)
+    return out, sel, s_hat, tau, mu, sigma, band, int(r_blk.sum())
 
 
 def forward(q, k, v, block_q: int, block_k: int, beta: float, mode: str,
             keep_tail_tokens: int = 0, query_blocks: Optional[Sequence[int]] = None,
             mask: Optional[np.ndarray] = None, heads: Optional[Sequence] = None,
-            workers: int = 0, threshold_mode: str = "exact") -> dict:
+            workers: int = 0, threshold_mode: str = "exact", causal_granule: int = 0) -> dict:
     """Sol-Attn forward pass for q, k, v of shape [B, H, N, d].
 
     mode: "dense" (Eq. dense_attn), "sparse" (exact selected blocks plus the
@@ -239,10 +318,12 @@ def forward(q, k, v, block_q: int, block_k: int, beta: float, mode: str,
     heads: optional list of (b, h) to evaluate (other heads NaN / empty).
     threshold_mode: "exact" (sigma_i from the full proxy row, equal to Eq.
     threshold_stats_exact) or "diagonal" (Appendix, Eq. appendix_diagonal_threshold).
+    causal_granule: 0 for bidirectional attention, G >= 1 for the causal mask
+    s < min((t // G + 1) G, N) (statistics over each query block's routable prefix).
 
     Returns a dict with out [B,H,N,d] float64, mask [B,H,NQ,NKr] bool, s_hat, tau,
     mu, sigma, frac [B,H] (kept fraction of routable pairs; 1.0 for dense) and
-    band [B,H] (pairs with |s_hat - tau| < 1e-3).
+    band [B,H] (routable pairs with |s_hat - tau| < 1e-3).
     """
     if mode not in MODES:
         raise ValueError(f"mode must be one of {MODES}")
@@ -254,6 +335,10 @@ def forward(q, k, v, block_q: int, block_k: int, beta: float, mode: str,
     B, H, n, d = q.shape
     if keep_tail_tokens % block_k:
         raise ValueError("keep_tail_tokens must be a multiple of block_k")
+    if causal_granule < 0:
+        raise ValueError("causal_granule must be >= 0")
+    if causal_granule and (keep_tail_tokens or threshold_mode != "exact"):
+        raise ValueError("causal masks take no forced tail and the exact threshold estimator only")
     n_forced = keep_tail_tokens // block_k
     nq = -(-n // block_q)
     nk = -(-n // block_k)
@@ -262,7 +347,7 @@ def forward(q, k, v, block_q: int, block_k: int, beta: float, mode: str,
     head_list = [(b, h) for b in range(B) for h in range(H)] if heads is None else list(heads)
 
     jobs = [(q[b, h], k[b, h], v[b, h], block_q, block_k, beta, mode, n_forced, qblocks,
-             None if mask is None else mask[b, h], threshold_mode) for b, h in head_list]
+             None if mask is None else mask[b, h], threshold_mode, causal_granule) for b, h in head_list]
     if workers and workers > 1 and len(jobs) > 1:
         with ProcessPoolExecutor(max_workers=min(workers, len(jobs))) as ex:
             results = list(ex.map(_forward_head, jobs))
@@ -279,22 +364,23 @@ def forward(q, k, v, block_q: int, block_k: int, beta: float, mode: str,
         "frac": np.full((B, H), np.nan),
         "band": np.zeros((B, H), dtype=np.int64),
     }
-    for (b, h), (out, sel, s_hat, tau, mu, sigma, band) in zip(head_list, results):
+    for (b, h), (out, sel, s_hat, tau, mu, sigma, band, n_routable) in zip(head_list, results):
         res["out"][b, h] = out
         res["mask"][b, h] = sel
         res["s_hat"][b, h] = s_hat
         res["tau"][b, h] = tau
         res["mu"][b, h] = mu
         res["sigma"][b, h] = sigma
-        res["frac"][b, h] = 1.0 if mode == "dense" else sel.mean()
+        res["frac"][b, h] = 1.0 if mode == "dense" else sel.sum() / max(n_routable, 1)
         res["band"][b, h] = band
     return res
 
 
 def routing(q, k, block_q: int, block_k: int, beta: float, keep_tail_tokens: int = 0,
-            threshold_mode: str = "exact") -> dict:
+            threshold_mode: str = "exact", causal_granule: int = 0) -> dict:
     """Routing only (pool -> proxies -> row statistics -> thresholds -> mask) for
-    all heads; cheap enough for the full 720p map."""
+    all heads; cheap enough for the full 720p map.  With causal_granule > 0 the
+    statistics and the mask cover each query block's routable prefix only."""
     q = np.asarray(q)
     k = np.asarray(k)
     d = q.shape[-1]
@@ -304,14 +390,30 @@ def routing(q, k, block_q: int, block_k: int, beta: float, keep_tail_tokens: int
     kbar, _ = pool_means(k, block_k)
     nkr = kbar.shape[-2] - n_forced
     s_hat = proxy_scores(qbar, kbar[..., :nkr, :], scale)
-    mu, sigma = row_stats(s_hat)
-    if threshold_mode == "diagonal":
-        sigma = diagonal_sigma(qbar, kbar[..., :nkr, :], scale)
-    tau = thresholds(mu, sigma, beta)
-    sel = route(s_hat, tau)
-    band = np.count_nonzero(np.abs(s_hat - tau[..., None]) < BAND, axis=(-1, -2))
+    if causal_granule:
+        if keep_tail_tokens or threshold_mode != "exact":
+            raise ValueError("causal masks take no forced tail and the exact threshold estimator only")
+        r_blk, _ = causal_block_ranges(q.shape[-2], block_q, block_k, causal_granule)
+        mu, sigma = causal_row_stats(s_hat.reshape(-1, nkr), np.tile(r_blk, s_hat.size // (len(r_blk) * nkr)))
+        mu, sigma = mu.reshape(s_hat.shape[:-1]), sigma.reshape(s_hat.shape[:-1])
+        tau = thresholds(mu, sigma, beta)
+        routable = np.arange(nkr)[None, :] < r_blk[:, None]
+        with np.errstate(invalid="ignore"):
+            sel = routable & (s_hat > tau[..., None])
+        n_routable = float(r_blk.sum())
+    else:
+        mu, sigma = row_stats(s_hat)
+        if threshold_mode == "diagonal":
+            sigma = diagonal_sigma(qbar, kbar[..., :nkr, :], scale)
+        tau = thresholds(mu, sigma, beta)
+        sel = route(s_hat, tau)
+        routable = np.ones(s_hat.shape[-2:], dtype=bool)
+        n_routable = float(routable.size)
+    with np.errstate(invalid="ignore"):
+        band = np.count_nonzero(routable & (np.abs(s_hat - tau[..., None]) < BAND), axis=(-1, -2))
     return {"mask": sel, "s_hat": s_hat, "tau": tau, "mu": mu, "sigma": sigma,
-            "frac": sel.mean(axis=(-1, -2)), "band": band, "qbar": qbar, "kbar": kbar}
+            "frac": sel.sum(axis=(-1, -2)) / n_routable, "band": band, "qbar": qbar, "kbar": kbar,
+            "routable": routable}
 
 
 def frac_selected(mask: np.ndarray) -> np.ndarray:

@@ -447,6 +447,171 @@ def test_hand_example():
     assert np.allclose(dn["out"], (1 + 2 * e**2 + 3 / e + 4 * e) / (1 + e**2 + 1 / e + e), atol=1e-14)
 
 
+# --------------------------------------------------------------------------- causal masks
+
+def causal_sdpa(q, k, v, granule):
+    n = q.shape[-2]
+    t = np.arange(n)
+    allowed = t[None, :] < np.minimum((t[:, None] // granule + 1) * granule, n)
+    return torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q), torch.from_numpy(k), torch.from_numpy(v),
+        attn_mask=torch.from_numpy(allowed)).numpy()
+
+
+@pytest.mark.parametrize("bq,bk,n,g", [(32, 16, 131, 1), (64, 64, 200, 1), (32, 16, 150, 40), (64, 16, 97, 13)])
+def test_causal_dense_and_full_selection_match_library_sdpa(bq, bk, n, g):
+    # Dense mode and beta = -inf (every routable block exact, partial blocks under the token
+    # mask) must both equal masked softmax attention from the library.
+    rng = np.random.default_rng(30)
+    q, k, v = rand_qkv(rng, N=n)
+    ref = causal_sdpa(q, k, v, g)
+    for mode, beta in (("dense", 0.3), ("sparse", -math.inf), ("sparse_no_correction", -math.inf)):
+        res = ora.forward(q, k, v, bq, bk, beta, mode, causal_granule=g)
+        assert np.max(np.abs(res["out"] - ref)) < 1e-12, mode
+
+
+def test_causal_block_ranges_brute_force():
+    # Classify every (query block, key block) pair by checking every (query, key) token
+    # pair: routable = seen by all rows, partial = seen by some rows.
+    for n, bq, bk, g in ((37, 8, 4, 1), (37, 8, 4, 3), (50, 16, 8, 20), (64, 16, 16, 16), (29, 8, 4, 100)):
+        r, e = ora.causal_block_ranges(n, bq, bk, g)
+        nq, nk = -(-n // bq), -(-n // bk)
+        for i in range(nq):
+            rows = range(i * bq, min((i + 1) * bq, n))
+            full, some = [], []
+            for j in range(nk):
+                keys = range(j * bk, min((j + 1) * bk, n))
+                seen = [(s // g) <= (t // g) for t in rows for s in keys]
+                full.append(all(seen))
+                some.append(any(seen))
+            assert full == [j < r[i] for j in range(nk)], (n, bq, bk, g, i)
+            assert some == [j < e[i] for j in range(nk)], (n, bq, bk, g, i)
+
+
+def _brute_causal(q, k, v, bq, bk, g, beta, mode):
+    """Pure-Python loops for one head: visibility from (s // g) <= (t // g), block
+    means, proxies, mean/std over the key blocks every row of the query block sees,
+    strict selection, then per-row exact terms over the visible keys of selected and
+    partially visible blocks plus n_j exp(q.Kbar_j) terms for unselected routable blocks."""
+    n, d = len(q), len(q[0])
+    sc = 1.0 / math.sqrt(d)
+    nq, nk = -(-n // bq), -(-n // bk)
+
+    def mean_rows(x, a, b):
+        return [sum(x[t][c] for t in range(a, b)) / (b - a) for c in range(d)]
+
+    def dot(a, b):
+        return sum(x * y for x, y in zip(a, b))
+
+    def vis(t, s):
+        return (s // g) <= (t // g)
+
+    kb = [(j * bk, min((j + 1) * bk, n)) for j in range(nk)]
+    kbar = [mean_rows(k, a, b) for a, b in kb]
+    out = [[0.0] * d for _ in range(n)]
+    mask = [[False] * nk for _ in range(nq)]
+    for i in range(nq):
+        r0, r1 = i * bq, min((i + 1) * bq, n)
+        qbar = mean_rows(q, r0, r1)
+        full = [all(vis(t, s) for t in range(r0, r1) for s in range(a, b)) for a, b in kb]
+        some = [any(vis(t, s) for t in range(r0, r1) for s in range(a, b)) for a, b in kb]
+        routable = [j for j in range(nk) if full[j]]
+        if routable:
+            sh = {j: sc * dot(qbar, kbar[j]) for j in routable}
+            mu = sum(sh.values()) / len(sh)
+            sig = math.sqrt(sum((x - mu) ** 2 for x in sh.values()) / len(sh))
+            tau = -math.inf if beta == -math.inf else (math.inf if beta == math.inf else mu + beta * sig)
+            for j in routable:
+                mask[i][j] = sh[j] > tau
+        for t in range(r0, r1):
+            terms = []   # (log weight, value vector)
+            for j in range(nk):
+                a, b = kb[j]
+                exact = some[j] and (mode == "dense" or not full[j] or mask[i][j])
+                if exact:
+                    for s in range(a, b):
+                        if vis(t, s):
+                            terms.append((sc * dot(q[t], k[s]), v[s]))
+                elif full[j] and mode == "sparse":
+                    vsum = [sum(v[s][c] for s in range(a, b)) for c in range(d)]
+                    terms.append((sc * dot(q[t], kbar[j]) + math.log(b - a), [x / (b - a) for x in vsum]))
+            if terms:
+                m = max(lw for lw, _ in terms)
+                den = sum(math.exp(lw - m) for lw, _ in terms)
+                out[t] = [sum(math.exp(lw - m) * vec[c] for lw, vec in terms) / den for c in range(d)]
+    return np.array(out), np.array(mask)
+
+
+@pytest.mark.parametrize("g", [1, 3, 12])
+@pytest.mark.parametrize("mode", ["sparse", "sparse_no_correction", "dense"])
+def test_causal_forward_brute_force(g, mode):
+    rng = np.random.default_rng(31)
+    n, d, bq, bk = 37, 4, 8, 4
+    q, k, v = smooth_qkv(rng, B=1, H=1, N=n, d=d)
+    for beta in (0.0, 0.7):
+        res = ora.forward(q, k, v, bq, bk, beta, mode, causal_granule=g)
+        out, mask = _brute_causal(q[0, 0].tolist(), k[0, 0].tolist(), v[0, 0].tolist(), bq, bk, g, beta, mode)
+        assert np.max(np.abs(res["out"][0, 0] - out)) < 1e-12
+        if mode != "dense":
+            assert (res["mask"][0, 0] == mask).all()
+
+
+def test_causal_granule_covering_the_sequence_is_bidirectional():
+    rng = np.random.default_rng(32)
+    q, k, v = smooth_qkv(rng, N=150)
+    for mode in ("sparse", "sparse_no_correction"):
+        a = ora.forward(q, k, v, 32, 16, 0.4, mode)
+        b = ora.forward(q, k, v, 32, 16, 0.4, mode, causal_granule=150)
+        assert (a["mask"] == b["mask"]).all()
+        assert np.max(np.abs(a["out"] - b["out"])) < 1e-13
+
+
+@pytest.mark.parametrize("g", [1, 24])
+def test_causal_outputs_ignore_future_keys(g):
+    # Rows of a query block must not depend on keys or values it cannot see: neither
+    # through the exact terms, nor through the routing statistics (centring over the
+    # visible blocks only), nor through the correction.  The future keys are pushed
+    # along the mean query so that their proxies, and any statistic that includes them,
+    # move far.
+    rng = np.random.default_rng(33)
+    n, bq, bk = 256, 32, 8
+    q, k, v = smooth_qkv(rng, N=n)
+    cut = 160
+    k2, v2 = k.copy(), v.copy()
+    qdir = q.mean(axis=-2, keepdims=True)
+    k2[..., cut:, :] += 4.0 * qdir + rng.standard_normal(k2[..., cut:, :].shape)
+    v2[..., cut:, :] = rng.standard_normal(v2[..., cut:, :].shape)
+    lim = ora.causal_limits(n, g)
+    keep = [i for i in range(-(-n // bq)) if lim[min((i + 1) * bq, n) - 1] <= cut]
+    assert len(keep) >= 4
+    for mode in ("sparse", "sparse_no_correction"):
+        a = ora.forward(q, k, v, bq, bk, 0.5, mode, causal_granule=g)
+        b = ora.forward(q, k2, v2, bq, bk, 0.5, mode, causal_granule=g)
+        rows = np.concatenate([np.arange(i * bq, min((i + 1) * bq, n)) for i in keep])
+        assert (a["mask"][:, :, keep] == b["mask"][:, :, keep]).all()
+        assert np.max(np.abs(a["out"][:, :, rows] - b["out"][:, :, rows])) < 1e-13
+
+
+def test_causal_weights_sum_to_one():
+    rng = np.random.default_rng(34)
+    q, k, _ = smooth_qkv(rng, N=130)
+    v = np.ones_like(q)
+    for g in (1, 20):
+        for mode in ("sparse", "dense"):
+            res = ora.forward(q, k, v, 32, 16, 0.8, mode, causal_granule=g)
+            assert np.max(np.abs(res["out"] - 1.0)) < 1e-12
+
+
+def test_causal_routing_matches_forward():
+    rng = np.random.default_rng(35)
+    q, k, v = smooth_qkv(rng, N=200)
+    r = ora.routing(q, k, 32, 16, 0.6, causal_granule=5)
+    f = ora.forward(q, k, v, 32, 16, 0.6, "sparse", causal_granule=5)
+    assert (r["mask"] == f["mask"]).all()
+    assert np.allclose(r["tau"], f["tau"], equal_nan=True)
+    assert np.allclose(r["frac"], f["frac"])
+
+
 # --------------------------------------------------------------------------- planted mistakes
 
 def test_pins_catch_a_dropped_multiplicity(monkeypatch):
@@ -488,3 +653,11 @@ def test_pins_catch_a_flipped_threshold_sign():
     expected = 1.0 - NormalDist().cdf(1.0)
     assert abs(float(r["frac"][0, 0]) - expected) < 0.015
     assert abs(float(wrong.mean()) - expected) > 0.5
+
+
+def test_pins_catch_causal_statistics_over_the_whole_row(monkeypatch):
+    # A plausible slip (centring the proxies over every key block instead of the
+    # visible ones) must break the future-keys pin.
+    monkeypatch.setattr(ora, "causal_row_stats", lambda s_hat, r: ora.row_stats(s_hat))
+    with pytest.raises(AssertionError):
+        test_causal_outputs_ignore_future_keys(1)
