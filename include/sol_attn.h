@@ -167,6 +167,34 @@ int sol_attn_forward_ex(const void* q, const void* k, const void* v, void* out,
                         void* workspace, size_t workspace_bytes,
                         uint32_t* counts, uint32_t* mask_out, void* stream);
 
+/*
+ * Routed attention forward under a causal mask (the row-dependent masks the
+ * Appendix's error analysis names as future work: they need centring and
+ * multiplicity over the valid keys).  Arguments as sol_attn_forward_ex, with no
+ * forced tail, plus:
+ *
+ * causal_granule (G >= 1): key s is visible to query t iff
+ *   s < min((t / G + 1) * G, N).  G = 1 is token-causal attention; G = the
+ *   tokens of one frame gives frame-causal (autoregressive video) attention;
+ *   G >= N is bidirectional attention.
+ *
+ * For query block i the key blocks every one of its rows sees are its routable
+ * blocks: mu_i and sigma_i are the mean and population deviation of the proxies
+ * over those blocks only (taken on chip from the proxies themselves), selection
+ * is s_hat_ij > mu_i + beta*sigma_i among them, and an unselected one enters the
+ * correction with its full valid-token count.  Key blocks only some rows see are
+ * computed exactly under the token mask; blocks no row sees are skipped.
+ * counts and mask_out cover the routable blocks only (mask bits of other blocks
+ * are 0); sol_attn_stats divides by the routable pairs of this mask.
+ * mode must not include SOL_THRESHOLD_DIAGONAL.  The workspace is the one
+ * sol_attn_workspace_bytes(..., keep_tail_tokens = 0) returns.
+ */
+int sol_attn_forward_causal(const void* q, const void* k, const void* v, void* out,
+                            int B, int H, int N, int d, int block_q, int block_k,
+                            float tau, int mode, int dtype, int causal_granule,
+                            void* workspace, size_t workspace_bytes,
+                            uint32_t* counts, uint32_t* mask_out, void* stream);
+
 /* Device workspace bytes sol_attn_forward_ex needs for these arguments, or 0
  * if they are invalid/unsupported. */
 size_t sol_attn_workspace_bytes(int B, int H, int N, int d, int block_q, int block_k,

@@ -29,6 +29,7 @@ SIGNATURES = {
     "sol_attn_thresholds": (_I, [_P, _P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _P]),
     "sol_attn_forward": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I]),
     "sol_attn_forward_ex": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _I, _I, _P, _S, _P, _P, _P]),
+    "sol_attn_forward_causal": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _I, _I, _P, _S, _P, _P, _P]),
     "sol_attn_workspace_bytes": (_S, [_I, _I, _I, _I, _I, _I, _I, _I, _I]),
     "sol_attn_stats": (_I, [_P, _I, _I]),
     "sol_attn_timing_enable": (_I, [_I]),
@@ -159,9 +160,11 @@ def workspace_bytes(B, H, N, d, block_q, block_k, mode, dtype=SOL_BF16, keep_tai
 
 
 def forward(q, k, v, block_q: int, block_k: int, tau: float, mode="sparse", keep_tail_tokens: int = 0,
-            out=None, workspace=None, counts=None, mask_out=None, threshold_mode: str = "exact"):
-    """Routed attention forward through sol_attn_forward_ex.  Returns out.
-    threshold_mode "diagonal" ORs SOL_THRESHOLD_DIAGONAL into the mode."""
+            out=None, workspace=None, counts=None, mask_out=None, threshold_mode: str = "exact",
+            causal_granule: int = 0):
+    """Routed attention forward through sol_attn_forward_ex, or sol_attn_forward_causal when
+    causal_granule > 0.  Returns out.  threshold_mode "diagonal" ORs SOL_THRESHOLD_DIAGONAL
+    into the mode."""
     import torch
     _check_qkv(q, k, v)
     B, H, N, d = q.shape
@@ -169,6 +172,13 @@ def forward(q, k, v, block_q: int, block_k: int, tau: float, mode="sparse", keep
         out = torch.empty_like(q)
     m = _mode_code(mode, threshold_mode)
     ws_ptr, ws_bytes = (None, 0) if workspace is None else (workspace.data_ptr(), workspace.numel() * workspace.element_size())
+    if causal_granule:
+        if keep_tail_tokens:
+            raise ValueError("causal masks take no forced tail")
+        _check(lib().sol_attn_forward_causal(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, block_q, block_k,
+                                             float(tau), m, _dtype_code(q), int(causal_granule), ws_ptr, ws_bytes,
+                                             _ptr(counts), _ptr(mask_out), _stream(q.device)))
+        return out
     _check(lib().sol_attn_forward_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, block_q, block_k,
                                      float(tau), m, _dtype_code(q), keep_tail_tokens, ws_ptr, ws_bytes,
                                      _ptr(counts), _ptr(mask_out), _stream(q.device)))

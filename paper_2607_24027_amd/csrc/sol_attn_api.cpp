@@ -2,6 +2,7 @@
 // launch sequencing.  Validation runs entirely on the host and returns before any HIP call.
 #include "../../include/sol_attn.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -50,7 +51,8 @@ std::map<int, DeviceBuffers> g_bufs;
 struct LastCall {
     bool valid = false;
     int device = 0;
-    int B = 0, H = 0, NQ = 0, NKr = 0;
+    int B = 0, H = 0;
+    double routable_pairs = 0.0;   // (query block, routable key block) pairs of one head
     const uint32_t* counts = nullptr;
     hipStream_t stream = nullptr;
 };
@@ -80,7 +82,7 @@ int check_common(int B, int H, int N, int d, int block_q, int block_k, int dtype
 }
 
 int validate_forward(const void* q, const void* k, const void* v, const void* out, int B, int H, int N, int d,
-                     int block_q, int block_k, float tau, int mode, int dtype, int keep_tail) {
+                     int block_q, int block_k, float tau, int mode, int dtype, int keep_tail, int causal_granule = 0) {
     if (!q || !k || !v || !out) return fail(SOL_ERR_INVALID_ARG, "q, k, v and out must be non-null");
     int rc = check_common(B, H, N, d, block_q, block_k, dtype);
     if (rc) return rc;
@@ -96,7 +98,12 @@ int validate_forward(const void* q, const void* k, const void* v, const void* ou
     if (keep_tail >= N && base != SOL_DENSE) return fail(SOL_ERR_INVALID_ARG, "keep_tail_tokens must leave at least one routable key block");
     if (keep_tail > N) return fail(SOL_ERR_INVALID_ARG, "keep_tail_tokens exceeds N");
     if (out == q || out == k || out == v) return fail(SOL_ERR_INVALID_ARG, "out must not alias q, k or v");
-    const sol::Shape s = sol::make_shape(B, H, N, d, block_q, block_k, mode, dtype, keep_tail);
+    if (causal_granule < 0) return fail(SOL_ERR_INVALID_ARG, "causal_granule must be >= 1 (got %d)", causal_granule);
+    if (causal_granule > 0 && (mode & SOL_THRESHOLD_DIAGONAL))
+        return fail(SOL_ERR_INVALID_ARG, "causal masks take their row statistics exactly; SOL_THRESHOLD_DIAGONAL is not supported");
+    if (causal_granule > 0 && keep_tail != 0)
+        return fail(SOL_ERR_INVALID_ARG, "causal masks take no forced tail");
+    const sol::Shape s = sol::make_shape(B, H, N, d, block_q, block_k, mode, dtype, keep_tail, causal_granule);
     if (sol::attn_lds_bytes(s) > (size_t)sol::kMaxLds)
         return fail(SOL_ERR_UNSUPPORTED, "sequence too long: %d key blocks exceed the on-chip routing list", s.NK);
     return SOL_OK;
@@ -187,12 +194,30 @@ size_t sol_attn_workspace_bytes(int B, int H, int N, int d, int block_q, int blo
     return sol::workspace_layout(s, nullptr, nullptr);
 }
 
-int sol_attn_forward_ex(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d, int block_q,
-                        int block_k, float tau, int mode, int dtype, int keep_tail_tokens, void* workspace,
-                        size_t workspace_bytes, uint32_t* counts, uint32_t* mask_out, void* stream) {
-    int rc = validate_forward(q, k, v, out, B, H, N, d, block_q, block_k, tau, mode, dtype, keep_tail_tokens);
+}  // extern "C"
+
+namespace {
+
+// Routable (query block, key block) pairs of one head: NQ * NKr, or under a causal mask the
+// sum over query blocks of the key blocks all their rows see.
+double routable_pairs(const sol::Shape& s) {
+    if (!s.causal) return (double)s.NQ * (double)s.NKr;
+    double tot = 0.0;
+    for (int i = 0; i < s.NQ; ++i) {
+        const long long t0 = (long long)i * s.bq;
+        const long long lo = std::min<long long>((t0 / s.causal + 1) * s.causal, s.N);
+        tot += lo >= s.N ? s.NK : (double)(lo / s.bk);
+    }
+    return tot;
+}
+
+int forward_impl(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d, int block_q,
+                 int block_k, float tau, int mode, int dtype, int keep_tail_tokens, int causal_granule,
+                 void* workspace, size_t workspace_bytes, uint32_t* counts, uint32_t* mask_out, void* stream) {
+    int rc = validate_forward(q, k, v, out, B, H, N, d, block_q, block_k, tau, mode, dtype, keep_tail_tokens,
+                              causal_granule);
     if (rc) return rc;
-    const sol::Shape s = sol::make_shape(B, H, N, d, block_q, block_k, mode, dtype, keep_tail_tokens);
+    const sol::Shape s = sol::make_shape(B, H, N, d, block_q, block_k, mode, dtype, keep_tail_tokens, causal_granule);
     const size_t need = sol::workspace_layout(s, nullptr, nullptr);
     if (workspace && workspace_bytes < need)
         return fail(SOL_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu bytes required", workspace_bytes, need);
@@ -248,11 +273,31 @@ int sol_attn_forward_ex(const void* q, const void* k, const void* v, void* out, 
     g_last.device = dev;
     g_last.B = B;
     g_last.H = H;
-    g_last.NQ = s.NQ;
-    g_last.NKr = s.NKr;
+    g_last.routable_pairs = routable_pairs(s);
     g_last.counts = counts;
     g_last.stream = st;
     return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int sol_attn_forward_ex(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d, int block_q,
+                        int block_k, float tau, int mode, int dtype, int keep_tail_tokens, void* workspace,
+                        size_t workspace_bytes, uint32_t* counts, uint32_t* mask_out, void* stream) {
+    return forward_impl(q, k, v, out, B, H, N, d, block_q, block_k, tau, mode, dtype, keep_tail_tokens, 0, workspace,
+                        workspace_bytes, counts, mask_out, stream);
+}
+
+int sol_attn_forward_causal(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d,
+                            int block_q, int block_k, float tau, int mode, int dtype, int causal_granule,
+                            void* workspace, size_t workspace_bytes, uint32_t* counts, uint32_t* mask_out,
+                            void* stream) {
+    if (causal_granule <= 0)
+        return fail(SOL_ERR_INVALID_ARG, "causal_granule must be >= 1 (got %d)", causal_granule);
+    return forward_impl(q, k, v, out, B, H, N, d, block_q, block_k, tau, mode, dtype, 0, causal_granule, workspace,
+                        workspace_bytes, counts, mask_out, stream);
 }
 
 int sol_attn_forward(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d, int block_q,
@@ -284,7 +329,7 @@ int sol_attn_stats(float* frac_per_head, int B, int H) {
         delete[] host;
         return hip_fail(e, "reading counts");
     }
-    const double denom = (double)last.NQ * (double)last.NKr;
+    const double denom = last.routable_pairs > 0.0 ? last.routable_pairs : 1.0;
     for (size_t i = 0; i < n; ++i) frac_per_head[i] = (float)((double)host[i] / denom);
     delete[] host;
     return ok();

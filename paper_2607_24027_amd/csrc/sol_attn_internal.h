@@ -22,11 +22,14 @@ struct Shape {
     int B, H, N, d, bq, bk;
     int mode, dtype, forced;       // forced = number of always-exact tail key blocks
     int diag;                      // 1: diagonal threshold estimator
+    int causal;                    // causal granule G (0: no mask); key s visible to query t iff
+                                   // s < min((t / G + 1) G, N)
     int BH, NQ, NK, NKr, NC, Npad, MW;
 };
 
 // `mode` is the ABI mode: base mode plus optional kThresholdDiagonal.
-Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype, int keep_tail_tokens);
+Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype, int keep_tail_tokens,
+                 int causal_granule = 0);
 
 // Workspace carve-up (all device pointers, 256-byte aligned inside one buffer).
 struct Workspace {

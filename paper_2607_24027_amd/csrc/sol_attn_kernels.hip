@@ -424,7 +424,30 @@ __global__ __launch_bounds__(256) void tau_kernel(const float* __restrict__ qbar
 // The online softmax is order independent, so running the correction tiles first changes
 // only the floating-point summation order.  Returns the number of exact tiles; *nuns
 // receives the number of unselected routable blocks and *nsel of selected ones.
+//
+// The routable blocks are [0, nr) and the forced ones [nr, ne): without a causal mask
+// nr = NKr and ne = NK (the forced tail).  With a causal mask (CAUSAL) [0, nr) are the key
+// blocks every row of the query block sees and [nr, ne) those only some rows see; the row
+// statistics then cover [0, nr) only and are taken here, from the proxies themselves: the
+// proxies go to LDS (prox, nr floats), their mean and population deviation give
+// tau_i = mu_i + beta sigma_i, and the selection bits follow.  (Prefix moments of the pooled
+// keys would need a d x d matrix per query block.)
 // ---------------------------------------------------------------------------
+
+// Sum over the workgroup; every thread gets the total.  scratch: NT/64 floats.
+template <int NT>
+__device__ float block_sum(float v, float* scratch) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    if (lane == 0) scratch[wave] = v;
+    __syncthreads();
+    float tot = 0.f;
+#pragma unroll
+    for (int w = 0; w < NT / 64; ++w) tot += scratch[w];
+    __syncthreads();
+    return tot;
+}
 
 template <int NT>
 __device__ int block_scan_incl(int v, int* scratch, int* total) {
@@ -449,10 +472,11 @@ __device__ int block_scan_incl(int v, int* scratch, int* total) {
     return v + pre;
 }
 
-template <int D, int NT, int MODE>
+template <int D, int NT, int MODE, bool CAUSAL = false>
 __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __restrict__ kbar_h, float tau_i,
-                              float scale, int NKr, int NK, int MW, int NC, uint32_t* selw, uint16_t* list,
-                              int* scan_scratch, int* nuns, int* nsel) {
+                              float beta, float scale, int NKr, int nr, int ne, int MW, float* prox, uint32_t* selw,
+                              uint16_t* list, int* scan_scratch, int* nuns, int* nsel) {
+    const int NC = (nr + kChunk - 1) / kChunk;   // chunks of routable blocks
     constexpr int CPR = D / 4;              // 16-byte chunks per f32 pooled-key row
     constexpr int TPK = NT / kChunk;        // threads per pooled key (1, 2 or 4)
     constexpr int CPT = CPR / TPK;          // 16-byte chunks of a row per thread
@@ -467,7 +491,7 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
 #pragma unroll
     for (int i = 0; i < CPT; ++i) qv[i] = *reinterpret_cast<const f32x4*>(qbar_i + 4 * (seg + TPK * i));
     auto load = [&](int c, f32x4 (&kv)[CPT]) SOL_INLINE {
-        const float* rp = kbar_h + (size_t)min(c * kChunk + jl, NKr - 1) * D;
+        const float* rp = kbar_h + (size_t)min(c * kChunk + jl, nr - 1) * D;
 #pragma unroll
         for (int i = 0; i < CPT; ++i) kv[i] = *reinterpret_cast<const f32x4*>(rp + 4 * (seg + TPK * i));
     };
@@ -484,7 +508,11 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
 #pragma unroll
         for (int off = 1; off < TPK; off <<= 1) dot += __shfl_xor(dot, off);
         const int j = c * kChunk + jl;
-        const bool sel = j < NKr && scale * dot > tau_i;
+        if constexpr (CAUSAL) {
+            if (seg == 0 && j < nr) prox[j] = scale * dot;
+            return;
+        }
+        const bool sel = j < nr && scale * dot > tau_i;
         const uint64_t bal = __ballot(sel);
         uint64_t bits = 0;
 #pragma unroll
@@ -517,6 +545,34 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
         }
     }
     __syncthreads();
+    if constexpr (CAUSAL) {
+        // row statistics over the routable prefix, then the selection bits of every word
+        float* fscratch = reinterpret_cast<float*>(scan_scratch);
+        float th = -kNegInf;
+        if (nr > 0) {
+            float acc = 0.f;
+            for (int j = tid; j < nr; j += NT) acc += prox[j];
+            const float mu = block_sum<NT>(acc, fscratch) / (float)nr;
+            acc = 0.f;
+            for (int j = tid; j < nr; j += NT) {
+                const float dv = prox[j] - mu;
+                acc = fmaf(dv, dv, acc);
+            }
+            const float sigma = sqrtf(block_sum<NT>(acc, fscratch) / (float)nr);
+            if (beta == kNegInf) th = kNegInf;
+            else if (beta == -kNegInf) th = -kNegInf;
+            else th = mu + beta * sigma;
+        }
+        for (int w = tid; w < MW; w += NT) {
+            uint32_t bits = 0u;
+            for (int b = 0; b < 32; ++b) {
+                const int j = 32 * w + b;
+                if (j < nr && prox[j] > th) bits |= 1u << b;
+            }
+            selw[w] = bits;
+        }
+        __syncthreads();
+    }
     auto chunk_bits = [&](int c) -> uint64_t {
         const uint32_t lo = selw[2 * c];
         const uint32_t hi = (2 * c + 1 < MW) ? selw[2 * c + 1] : 0u;
@@ -531,7 +587,7 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
             const int c = c0 + tid;
             uint64_t ub = 0;
             if (c < NC) {
-                const int nvalid = min(kChunk, NKr - c * kChunk);
+                const int nvalid = min(kChunk, nr - c * kChunk);
                 const uint64_t valid = nvalid >= 64 ? ~0ull : ((1ull << nvalid) - 1ull);
                 ub = ~chunk_bits(c) & valid;
             }
@@ -563,11 +619,11 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
         }
         n_sel += tot;
     }
-    for (int j = NKr + tid; j < NK; j += NT) elist[n_sel + (j - NKr)] = (uint16_t)j;
+    for (int j = nr + tid; j < ne; j += NT) elist[n_sel + (j - nr)] = (uint16_t)j;
     __syncthreads();
     *nuns = n_uns;
     *nsel = n_sel;
-    return n_sel + (NK - NKr);
+    return n_sel + (ne - nr);
 }
 
 // ---------------------------------------------------------------------------
@@ -588,7 +644,20 @@ struct AttnArgs {
     int BH, N, NQ, NK, NKr, NC, MW, per_x;
     float scale, c_log2;
     float bias_full, bias_last;   // log2(n_j)/c_log2 for full blocks and for the last block
+    int causal_g;                 // causal granule G (CAUSAL kernels): key s visible to query t iff s < lim(t)
+    float beta;                   // standardised cutoff (CAUSAL kernels take tau_i on chip)
 };
+
+// Causal masks: query t sees the keys s < lim(t) = min((t / G + 1) G, N).  For query block qi
+// of BQ rows, [0, nr) are the key blocks all its rows see and [nr, ne) those some rows see.
+__device__ __forceinline__ int causal_lim(int t, int G, int N) { return min((t / G + 1) * G, N); }
+template <int BQ>
+__device__ __forceinline__ void causal_ranges(int qi, int G, int N, int NK, int& nr, int& ne) {
+    const int lo = causal_lim(qi * BQ, G, N);
+    const int hi = causal_lim(min((qi + 1) * BQ, N) - 1, G, N);
+    nr = lo >= N ? NK : lo / kBlockK;
+    ne = (hi + kBlockK - 1) / kBlockK;
+}
 
 // LDS tiles of the fused kernel, without padding.  gfx950 serves a ds_read_b128 16 lanes per
 // cycle from 64 banks, so 16 consecutive MFMA rows reading the same 16-byte chunk column must
@@ -674,7 +743,7 @@ __device__ __forceinline__ void lds_copy16(const void* src, lds_ptr_t dst) {
 template <int D, int BQ>
 constexpr int kAttnWavesPerEU = (D == 128 && BQ == 64) ? 1 : 2;
 
-template <int D, int BQ, int MODE>
+template <int D, int BQ, int MODE, bool CAUSAL>
 __global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(kAttnWavesPerEU<D, BQ>, kAttnWavesPerEU<D, BQ>)))
 void routed_attn_kernel(AttnArgs a) {
     constexpr int NT = BQ * 2;            // 64 threads per 32 query rows
@@ -687,11 +756,20 @@ void routed_attn_kernel(AttnArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
 
     // XCD-aware mapping: consecutive workgroups go round-robin to the 8 XCDs, so XCD x gets
-    // a contiguous range of query blocks of the current head.
+    // a contiguous range of query blocks of the current head.  Under a causal mask the work
+    // of a query block grows with its index, so the head's blocks are cut into 16 segments
+    // and XCD x takes segment 15 - x (descending, the longer blocks first) and then segment
+    // x: every XCD gets the same amount of work.
     const int wg = blockIdx.x;
     const int xcd = wg & 7, y = wg >> 3;
     const int bh = y / a.per_x;
-    const int qi = xcd * a.per_x + (y % a.per_x);
+    int qi;
+    if constexpr (CAUSAL) {
+        const int u = y % a.per_x, hp = a.per_x >> 1;
+        qi = u < hp ? (15 - xcd) * hp + (hp - 1 - u) : xcd * hp + (u - hp);
+    } else {
+        qi = xcd * a.per_x + (y % a.per_x);
+    }
     if (bh >= a.BH || qi >= a.NQ) return;
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -702,17 +780,21 @@ void routed_attn_kernel(AttnArgs a) {
     int* scan_scratch = reinterpret_cast<int*>(rest);
     uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64);
     uint16_t* list = reinterpret_cast<uint16_t*>(rest + 64 + 4 * ((a.MW + 3) & ~3));
+    float* prox = reinterpret_cast<float*>(rest + ((64 + 4 * ((a.MW + 3) & ~3) + 2 * (a.NKr + a.NK) + 15) & ~15));
     const uint16_t* ulist = list;            // correction slots (unselected routable blocks)
     const uint16_t* elist = list + a.NKr;    // exact tiles
 
+    int nr = a.NKr, ne = a.NK;               // routable blocks [0, nr), forced blocks [nr, ne)
+    if constexpr (CAUSAL) causal_ranges<BQ>(qi, a.causal_g, a.N, a.NK, nr, ne);
     int ntiles, nsel, nuns = 0;
     if (MODE == kDense) {
-        ntiles = a.NK;
-        nsel = a.NKr;
+        ntiles = ne;
+        nsel = nr;
     } else {
-        ntiles = route_and_list<D, NT, MODE>(a.qbar + ((size_t)bh * a.NQ + qi) * D, a.kbar + (size_t)bh * a.NK * D,
-                                             a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, selw,
-                                             list, scan_scratch, &nuns, &nsel);
+        const float tau_i = CAUSAL ? 0.f : a.tau[(size_t)bh * a.NQ + qi];
+        ntiles = route_and_list<D, NT, MODE, CAUSAL>(a.qbar + ((size_t)bh * a.NQ + qi) * D,
+                                                     a.kbar + (size_t)bh * a.NK * D, tau_i, a.beta, a.scale, a.NKr,
+                                                     nr, ne, a.MW, prox, selw, list, scan_scratch, &nuns, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
@@ -723,6 +805,7 @@ void routed_attn_kernel(AttnArgs a) {
 
     const int qrow = qi * BQ + wave * 32 + r32;
     const uint16_t* qrow_p = a.q + ((size_t)bh * a.N + min(qrow, a.N - 1)) * D + 8 * hh;
+    const int qlim = CAUSAL ? causal_lim(qrow, a.causal_g, a.N) : a.N;   // this lane's query sees keys < qlim
 
     f32x16 o[NDT];
 #pragma unroll
@@ -902,6 +985,16 @@ void routed_attn_kernel(AttnArgs a) {
             }
         }
     };
+    // Causal mask of a partially visible key block j: keys at or past this lane's limit -> -inf.
+    auto mask_causal = [&](int j, f32x16& s0, f32x16& s1) SOL_INLINE {
+        const int rel = qlim - j * kBlockK;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int key0 = 8 * (r >> 2) + 4 * hh + (r & 3);
+            if (key0 >= rel) s0[r] = kNegInf;
+            if (32 + key0 >= rel) s1[r] = kNegInf;
+        }
+    };
     // Correction tile of chunk c: slot j contributes with log2(n_j) (the multiplicity of Eq.
     // solattn_denominator) unless it is selected (exact tile) or past the routable keys.
     auto bias_apx = [&](int c, f32x16& s0, f32x16& s1) SOL_INLINE {
@@ -1020,9 +1113,15 @@ void routed_attn_kernel(AttnArgs a) {
             if constexpr (APX) return __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bq, acc, 0, 0, 0);
             else return __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bq, acc, 0, 0, 0);
         };
-        // scores of tile t are complete: add the correction bias (correction tiles)
+        // scores of tile t are complete: add the correction bias (correction tiles), or mask the
+        // keys a row does not see (exact tiles of partially visible blocks, causal masks)
         auto scores_done = [&](int t, f32x16& s0, f32x16& s1) SOL_INLINE {
-            if constexpr (APX) bias_apx(code(t), s0, s1);
+            if constexpr (APX) {
+                bias_apx(code(t), s0, s1);
+            } else if constexpr (CAUSAL) {
+                const int j = code(t);
+                if (j >= nr) mask_causal(j, s0, s1);
+            }
         };
         issue_k(0, 0);
         issue_v(0, 0);
@@ -1208,9 +1307,11 @@ struct AttnArgsF32 {
     uint32_t* mask_out;
     int BH, N, NQ, NK, NKr, NC, MW;
     float scale;
+    int causal_g;
+    float beta;
 };
 
-template <int D, int BQ, int MODE>
+template <int D, int BQ, int MODE, bool CAUSAL>
 __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
     constexpr int NT = BQ;
     extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -1221,24 +1322,29 @@ __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
     int* scan_scratch = reinterpret_cast<int*>(rest);
     uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64);
     uint16_t* list = reinterpret_cast<uint16_t*>(rest + 64 + 4 * ((a.MW + 3) & ~3));
+    float* prox = reinterpret_cast<float*>(rest + ((64 + 4 * ((a.MW + 3) & ~3) + 2 * (a.NKr + a.NK) + 15) & ~15));
     const uint16_t* ulist = list;            // correction slots (unselected routable blocks)
     const uint16_t* elist = list + a.NKr;    // exact tiles
 
     const int bh = blockIdx.y, qi = blockIdx.x, tid = threadIdx.x;
+    int nr = a.NKr, ne = a.NK;               // routable blocks [0, nr), forced blocks [nr, ne)
+    if constexpr (CAUSAL) causal_ranges<BQ>(qi, a.causal_g, a.N, a.NK, nr, ne);
     int ntiles, nsel, nuns = 0;
     if (MODE == kDense) {
-        ntiles = a.NK;
-        nsel = a.NKr;
+        ntiles = ne;
+        nsel = nr;
     } else {
-        ntiles = route_and_list<D, NT, MODE>(a.qbar + ((size_t)bh * a.NQ + qi) * D, a.kbar + (size_t)bh * a.NK * D,
-                                             a.tau[(size_t)bh * a.NQ + qi], a.scale, a.NKr, a.NK, a.MW, a.NC, selw,
-                                             list, scan_scratch, &nuns, &nsel);
+        const float tau_i = CAUSAL ? 0.f : a.tau[(size_t)bh * a.NQ + qi];
+        ntiles = route_and_list<D, NT, MODE, CAUSAL>(a.qbar + ((size_t)bh * a.NQ + qi) * D,
+                                                     a.kbar + (size_t)bh * a.NK * D, tau_i, a.beta, a.scale, a.NKr,
+                                                     nr, ne, a.MW, prox, selw, list, scan_scratch, &nuns, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
     if (tid == 0) a.blkcount[(size_t)bh * a.NQ + qi] = (uint32_t)nsel;
 
     const int row = qi * BQ + tid;
+    const int qlim = CAUSAL ? causal_lim(row, a.causal_g, a.N) : a.N;   // this row sees keys < qlim
     for (int e = tid; e < BQ * D; e += NT) {
         const int rr = e / D, c = e % D, gr = qi * BQ + rr;
         qt[c * BQ + rr] = gr < a.N ? a.q[((size_t)bh * a.N + gr) * D + c] : 0.f;
@@ -1281,7 +1387,7 @@ __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
                 if (c * kChunk + u >= nuns) continue;
                 const int j = ulist[c * kChunk + u];
                 bias = logf((float)min(kBlockK, a.N - j * kBlockK));
-            } else if (c * kBlockK + u >= a.N) {
+            } else if (c * kBlockK + u >= (CAUSAL && c >= nr ? qlim : a.N)) {
                 continue;
             }
             float dot = 0.f;
@@ -1328,10 +1434,10 @@ hipError_t allow_lds(K kernel, size_t bytes) {
                                (int)bytes);
 }
 
-template <int D, int BQ, int MODE>
+template <int D, int BQ, int MODE, bool CAUSAL>
 hipError_t launch_attn_bf16(const Shape& s, const AttnArgs& a, hipStream_t st) {
     const size_t lds = attn_lds_bytes(s);
-    auto kern = routed_attn_kernel<D, BQ, MODE>;
+    auto kern = routed_attn_kernel<D, BQ, MODE, CAUSAL>;
     hipError_t e = allow_lds(kern, lds);
     if (e != hipSuccess) return e;
     const int grid = 8 * a.per_x * a.BH;
@@ -1339,32 +1445,42 @@ hipError_t launch_attn_bf16(const Shape& s, const AttnArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
-template <int D, int BQ, int MODE>
+template <int D, int BQ, int MODE, bool CAUSAL>
 hipError_t launch_attn_f32(const Shape& s, const AttnArgsF32& a, hipStream_t st) {
     const size_t lds = attn_lds_bytes(s);
-    auto kern = routed_attn_f32_kernel<D, BQ, MODE>;
+    auto kern = routed_attn_f32_kernel<D, BQ, MODE, CAUSAL>;
     hipError_t e = allow_lds(kern, lds);
     if (e != hipSuccess) return e;
     kern<<<dim3(a.NQ, a.BH), dim3(BQ), lds, st>>>(a);
     return hipGetLastError();
 }
 
-template <int D, int BQ>
+template <int D, int BQ, bool CAUSAL>
 hipError_t dispatch_bf16_mode(const Shape& s, const AttnArgs& a, hipStream_t st) {
     switch (s.mode) {
-        case kDense: return launch_attn_bf16<D, BQ, kDense>(s, a, st);
-        case kSparse: return launch_attn_bf16<D, BQ, kSparse>(s, a, st);
-        default: return launch_attn_bf16<D, BQ, kSparseNoCorr>(s, a, st);
+        case kDense: return launch_attn_bf16<D, BQ, kDense, CAUSAL>(s, a, st);
+        case kSparse: return launch_attn_bf16<D, BQ, kSparse, CAUSAL>(s, a, st);
+        default: return launch_attn_bf16<D, BQ, kSparseNoCorr, CAUSAL>(s, a, st);
     }
 }
 
 template <int D, int BQ>
+hipError_t dispatch_bf16(const Shape& s, const AttnArgs& a, hipStream_t st) {
+    return s.causal ? dispatch_bf16_mode<D, BQ, true>(s, a, st) : dispatch_bf16_mode<D, BQ, false>(s, a, st);
+}
+
+template <int D, int BQ, bool CAUSAL>
 hipError_t dispatch_f32_mode(const Shape& s, const AttnArgsF32& a, hipStream_t st) {
     switch (s.mode) {
-        case kDense: return launch_attn_f32<D, BQ, kDense>(s, a, st);
-        case kSparse: return launch_attn_f32<D, BQ, kSparse>(s, a, st);
-        default: return launch_attn_f32<D, BQ, kSparseNoCorr>(s, a, st);
+        case kDense: return launch_attn_f32<D, BQ, kDense, CAUSAL>(s, a, st);
+        case kSparse: return launch_attn_f32<D, BQ, kSparse, CAUSAL>(s, a, st);
+        default: return launch_attn_f32<D, BQ, kSparseNoCorr, CAUSAL>(s, a, st);
     }
+}
+
+template <int D, int BQ>
+hipError_t dispatch_f32(const Shape& s, const AttnArgsF32& a, hipStream_t st) {
+    return s.causal ? dispatch_f32_mode<D, BQ, true>(s, a, st) : dispatch_f32_mode<D, BQ, false>(s, a, st);
 }
 
 }  // namespace
@@ -1372,8 +1488,10 @@ hipError_t dispatch_f32_mode(const Shape& s, const AttnArgsF32& a, hipStream_t s
 // ---------------------------------------------------------------------------
 // Host-side launch helpers
 // ---------------------------------------------------------------------------
-Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype, int keep_tail_tokens) {
+Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype, int keep_tail_tokens,
+                 int causal_granule) {
     Shape s{};
+    s.causal = causal_granule;
     s.B = B; s.H = H; s.N = N; s.d = d; s.bq = bq; s.bk = bk;
     s.mode = mode & ~kThresholdDiagonal; s.dtype = dtype;
     s.diag = (mode & kThresholdDiagonal) ? 1 : 0;
@@ -1389,7 +1507,8 @@ Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype
 }
 
 size_t attn_lds_bytes(const Shape& s) {
-    const size_t rest = 64 + 4 * (size_t)((s.MW + 3) & ~3) + 2 * (size_t)(s.NKr + s.NK);
+    size_t rest = 64 + 4 * (size_t)((s.MW + 3) & ~3) + 2 * (size_t)(s.NKr + s.NK);
+    if (s.causal && s.mode != kDense) rest = ((rest + 15) & ~(size_t)15) + 4 * (size_t)s.NKr;   // proxies of a row
     if (s.dtype == kBF16) {
         const size_t stage = (size_t)kBlockK * s.d * 2 * 2;
         return 2 * stage + rest;
@@ -1492,9 +1611,13 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         if ((e = hipGetLastError()) != hipSuccess) return e;
         if (routing) {
             if ((e = launch_pool_mean(q, ws.qbar, kBF16, s.BH, s.N, d, s.bq, st)) != hipSuccess) return e;
-            if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, ws.mom, s.BH, s.NK, s.NKr, d, st)) != hipSuccess) return e;
-            if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, s.diag, st)) != hipSuccess)
-                return e;
+            if (!s.causal) {   // causal masks: the kernel takes each row's statistics itself
+                if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, ws.mom, s.BH, s.NK, s.NKr, d, st)) != hipSuccess)
+                    return e;
+                if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, s.diag,
+                                    st)) != hipSuccess)
+                    return e;
+            }
         }
         AttnArgs a{};
         a.q = static_cast<const uint16_t*>(q);
@@ -1509,14 +1632,16 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         a.blkcount = ws.blkcount;
         a.mask_out = mask_out;
         a.BH = s.BH; a.N = s.N; a.NQ = s.NQ; a.NK = s.NK; a.NKr = s.NKr; a.NC = s.NC; a.MW = s.MW;
-        a.per_x = (s.NQ + 7) / 8;
+        a.per_x = s.causal ? 2 * ((s.NQ + 15) / 16) : (s.NQ + 7) / 8;
         a.scale = scale;
+        a.causal_g = s.causal;
+        a.beta = beta;
         a.c_log2 = scale * kLog2e;
         a.bias_full = log2f((float)kBlockK) / a.c_log2;
         a.bias_last = log2f((float)(s.N - (s.NK - 1) * kBlockK)) / a.c_log2;
         if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
-        if (d == 128) e = s.bq == 128 ? dispatch_bf16_mode<128, 128>(s, a, st) : dispatch_bf16_mode<128, 64>(s, a, st);
-        else e = s.bq == 128 ? dispatch_bf16_mode<64, 128>(s, a, st) : dispatch_bf16_mode<64, 64>(s, a, st);
+        if (d == 128) e = s.bq == 128 ? dispatch_bf16<128, 128>(s, a, st) : dispatch_bf16<128, 64>(s, a, st);
+        else e = s.bq == 128 ? dispatch_bf16<64, 128>(s, a, st) : dispatch_bf16<64, 64>(s, a, st);
         if (e != hipSuccess) return e;
         if (ev_stop && (e = hipEventRecord(ev_stop, st)) != hipSuccess) return e;
     } else {
@@ -1525,9 +1650,13 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
             if ((e = launch_pool_mean(k, ws.kbar, kF32, s.BH, s.N, d, s.bk, st)) != hipSuccess) return e;
             if (s.mode == kSparse && (e = launch_pool_mean(v, ws.vbar, kF32, s.BH, s.N, d, s.bk, st)) != hipSuccess)
                 return e;
-            if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, ws.mom, s.BH, s.NK, s.NKr, d, st)) != hipSuccess) return e;
-            if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, s.diag, st)) != hipSuccess)
-                return e;
+            if (!s.causal) {
+                if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, ws.mom, s.BH, s.NK, s.NKr, d, st)) != hipSuccess)
+                    return e;
+                if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, s.diag,
+                                    st)) != hipSuccess)
+                    return e;
+            }
         }
         AttnArgsF32 a{};
         a.q = static_cast<const float*>(q);
@@ -1542,9 +1671,11 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         a.mask_out = mask_out;
         a.BH = s.BH; a.N = s.N; a.NQ = s.NQ; a.NK = s.NK; a.NKr = s.NKr; a.NC = s.NC; a.MW = s.MW;
         a.scale = scale;
+        a.causal_g = s.causal;
+        a.beta = beta;
         if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
-        if (d == 128) e = s.bq == 128 ? dispatch_f32_mode<128, 128>(s, a, st) : dispatch_f32_mode<128, 64>(s, a, st);
-        else e = s.bq == 128 ? dispatch_f32_mode<64, 128>(s, a, st) : dispatch_f32_mode<64, 64>(s, a, st);
+        if (d == 128) e = s.bq == 128 ? dispatch_f32<128, 128>(s, a, st) : dispatch_f32<128, 64>(s, a, st);
+        else e = s.bq == 128 ? dispatch_f32<64, 128>(s, a, st) : dispatch_f32<64, 64>(s, a, st);
         if (e != hipSuccess) return e;
         if (ev_stop && (e = hipEventRecord(ev_stop, st)) != hipSuccess) return e;
     }
