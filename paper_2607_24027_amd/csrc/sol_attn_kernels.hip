@@ -40,6 +40,7 @@ constexpr float kLog2e = 1.4426950408889634f;
 // Lazy rescaling: the running max subtracted from the logits (log2 units) is only raised
 // when a tile's max exceeds it by more than this, so probabilities stay <= 2^8 (f16-safe).
 constexpr float kRescaleSlack = 8.0f;
+constexpr float kLog2BlockK = 6.0f;   // log2(64): multiplicity of a full key block, log2 units
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t bits16) {
     return __uint_as_float(bits16 << 16);
@@ -732,9 +733,11 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const char* p) {
 // otherwise treat every later LDS read as possibly aliasing an in-flight copy, is left free
 // to schedule the operand reads.  dst must be wave-uniform (it goes to m0); the s_nop covers
 // the one-wait-state hazard between an m0 write and an LDS DMA that reads it.
-__device__ __forceinline__ void lds_copy16(const void* src, lds_ptr_t dst) {
+// The address is a wave-uniform base (scalar registers) plus a per-lane 32-bit byte offset,
+// so no per-lane 64-bit address arithmetic is needed.
+__device__ __forceinline__ void lds_copy16(const void* base, uint32_t off, lds_ptr_t dst) {
     const uint32_t m0 = (uint32_t)(uintptr_t)dst;
-    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(m0) : "memory");
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(m0) : "memory");
 }
 
 // Waves per SIMD the attention kernel is register-budgeted for: two, except where the LDS of a
@@ -857,6 +860,9 @@ void routed_attn_kernel(AttnArgs a) {
     const char* vbh_base = reinterpret_cast<const char*>(a.vbarh + (size_t)bh * a.NC * kChunk * D);
     auto issue_apx_k = [&](int c, int buf) SOL_INLINE {
         char* stage = smem + buf * L::STAGE;
+        // all row lookups first, so that they are in flight together (each copy is ordered
+        // after every memory access before it)
+        uint32_t off[KPW];
 #pragma unroll
         for (int u = 0; u < KPW; ++u) {
             int r, cc;
@@ -866,9 +872,10 @@ void routed_attn_kernel(AttnArgs a) {
             } else {
                 L::ksrc((wave * KPW + u) * 64 + lane, r, cc);
             }
-            lds_copy16(kbh_base + ((size_t)slot_row(c, r) * D + cc * 8) * 2,
-                       (lds_ptr_t)(stage + (wave * KPW + u) * 1024));
+            off[u] = (uint32_t)(slot_row(c, r) * D + cc * 8) * 2u;
         }
+#pragma unroll
+        for (int u = 0; u < KPW; ++u) lds_copy16(kbh_base, off[u], (lds_ptr_t)(stage + (wave * KPW + u) * 1024));
     };
     // ... and the f16 value means of the same rows into its V region, row-major (slot s at
     // s * 2D bytes, 16-byte chunk q of a row holding chunk q ^ rswz(s)), read back transposed
@@ -877,39 +884,44 @@ void routed_attn_kernel(AttnArgs a) {
         char* stage = smem + buf * L::STAGE;
         constexpr int LPR = L::RCPR;                  // lanes per row of a copy
         const int cc = (lane % LPR) ^ L::rswz(lane / LPR);   // rswz depends on the row mod 4
+        uint32_t off[VPW];
 #pragma unroll
         for (int u = 0; u < VPW; ++u) {
             const int r = (64 / LPR) * (wave * VPW + u) + lane / LPR;
-            lds_copy16(vbh_base + ((size_t)slot_row(c, r) * D + cc * 8) * 2,
-                       (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024));
+            off[u] = (uint32_t)(slot_row(c, r) * D + cc * 8) * 2u;
         }
+#pragma unroll
+        for (int u = 0; u < VPW; ++u)
+            lds_copy16(vbh_base, off[u], (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024));
     };
     // ... and of an exact tile: key block j into stage `buf`'s K region ...
     auto issue_exact_k = [&](int j, int buf) SOL_INLINE {
+        j = __builtin_amdgcn_readfirstlane(j);   // the same block for every lane: scalar base address
         char* stage = smem + buf * L::STAGE;
         const char* kp = reinterpret_cast<const char*>(a.k + ((size_t)bh * a.N + (size_t)j * kBlockK) * D);
         const int nrows = a.N - j * kBlockK;
         if (nrows >= kBlockK) {
 #pragma unroll
             for (int u = 0; u < KPW; ++u)
-                lds_copy16(kp + kofs(u), (lds_ptr_t)(stage + (wave * KPW + u) * 1024));
+                lds_copy16(kp, kofs(u), (lds_ptr_t)(stage + (wave * KPW + u) * 1024));
         } else {
 #pragma unroll
             for (int u = 0; u < KPW; ++u) {
                 int r, c;
                 L::ksrc((wave * KPW + u) * 64 + lane, r, c);
                 const uint32_t off = (uint32_t)(min(r, nrows - 1) * D + c * 8) * 2u;
-                lds_copy16(kp + off, (lds_ptr_t)(stage + (wave * KPW + u) * 1024));
+                lds_copy16(kp, off, (lds_ptr_t)(stage + (wave * KPW + u) * 1024));
             }
         }
     };
     // ... and its transposed values into stage `buf`'s V region.
     auto issue_exact_v = [&](int j, int buf) SOL_INLINE {
+        j = __builtin_amdgcn_readfirstlane(j);
         char* stage = smem + buf * L::STAGE;
         const char* vp = reinterpret_cast<const char*>(a.vt + ((size_t)bh * a.NK + j) * D * kBlockK);
 #pragma unroll
         for (int u = 0; u < VPW; ++u)
-            lds_copy16(vp + vofs(u), (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024));
+            lds_copy16(vp, vofs(u), (lds_ptr_t)(stage + L::KBYTES + (wave * VPW + u) * 1024));
     };
 
     const float cl = a.c_log2;
@@ -1018,16 +1030,26 @@ void routed_attn_kernel(AttnArgs a) {
     // Online softmax in the log2 domain with lazy rescaling, split so that the (rarely
     // taken) rescale branch sits apart from the MFMA/VALU stream:
     //   tile_max  - row max of a score tile (both lane halves of a query agree)
-    //   rescale   - raise the running max if a tile exceeds it by more than kRescaleSlack
-    //   exps      - P^T = exp2(S*c - m) packed as f16 B operands; row sums from the rounded P
+    //   rescale   - raise the running max (log2 units) if a tile's max exceeds it by more than
+    //               kRescaleSlack
+    //   exps      - P^T = exp2(S*c + bo - m) packed as f16 B operands; row sums from the rounded
+    //               P.  bo is a per-tile exponent offset: log2(64) for correction tiles whose
+    //               64 slots are all full routable blocks (their multiplicity), else 0.
     auto tile_max = [&](const f32x16& s0, const f32x16& s1) SOL_INLINE -> float {
-        float mx = kNegInf;
+        // balanced tree over the lane's 32 scores (short dependency chains) ...
+        float m[16];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, fmaxf(s0[r], s1[r]));
-        return fmaxf(mx, __shfl_xor(mx, 32));
+        for (int r = 0; r < 16; ++r) m[r] = fmaxf(s0[r], s1[r]);
+#pragma unroll
+        for (int w = 8; w > 0; w >>= 1)
+#pragma unroll
+            for (int r = 0; r < w; ++r) m[r] = fmaxf(m[r], m[r + w]);
+        // ... then across the lane pair (l, l+32) that holds the query's other 32 keys, with a
+        // VALU lane swap instead of an LDS permute
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(m[0]), __float_as_uint(m[0]), false, false);
+        return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
     };
-    auto rescale = [&](float mx) SOL_INLINE {
-        const float mt_ = mx * cl;
+    auto rescale = [&](float mt_) SOL_INLINE {
         const bool need = mt_ > m_run + kRescaleSlack;
         if (__ballot(need)) {
             const float mnew = need ? mt_ : m_run;
@@ -1038,8 +1060,8 @@ void routed_attn_kernel(AttnArgs a) {
             m_run = mnew;
         }
     };
-    auto exps = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[4]) SOL_INLINE {
-        const float msub = m_run == kNegInf ? 0.f : m_run;
+    auto exps = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[4], float bo) SOL_INLINE {
+        const float msub = (m_run == kNegInf ? 0.f : m_run) - bo;
         const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
 #pragma unroll
         for (int tt = 0; tt < 2; ++tt) {
@@ -1060,9 +1082,9 @@ void routed_attn_kernel(AttnArgs a) {
             }
         }
     };
-    auto softmax = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[4]) SOL_INLINE {
-        rescale(tile_max(s0, s1));
-        exps(s0, s1, pb);
+    auto softmax = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[4], float bo) SOL_INLINE {
+        rescale(tile_max(s0, s1) * cl + bo);
+        exps(s0, s1, pb, bo);
     };
     // O^T += V^T P^T, operands double-buffered in registers.
     auto pv = [&](auto apx_tag, auto stage_tag, const f16x8 (&pb)[4]) SOL_INLINE {
@@ -1101,37 +1123,57 @@ void routed_attn_kernel(AttnArgs a) {
     auto pipeline = [&](auto apx_tag, const auto& qop, const int T, auto code) SOL_INLINE {
         constexpr bool APX = decltype(apx_tag)::value;
         using KT = std::conditional_t<APX, f16x8, bf16x8>;
-        auto issue_k = [&](int t, int buf) SOL_INLINE {
-            if constexpr (APX) issue_apx_k(code(t), buf);
-            else issue_exact_k(code(t), buf);
+        // copies of the tile with code c (its key block, or its correction chunk)
+        auto issue_k = [&](int c, int buf) SOL_INLINE {
+            if constexpr (APX) issue_apx_k(c, buf);
+            else issue_exact_k(c, buf);
         };
-        auto issue_v = [&](int t, int buf) SOL_INLINE {
-            if constexpr (APX) issue_apx_v(code(t), buf);
-            else issue_exact_v(code(t), buf);
+        auto issue_v = [&](int c, int buf) SOL_INLINE {
+            if constexpr (APX) issue_apx_v(c, buf);
+            else issue_exact_v(c, buf);
         };
         auto mfma_qk = [](const KT& av, const KT& bq, const f32x16& acc) SOL_INLINE {
             if constexpr (APX) return __builtin_amdgcn_mfma_f32_32x32x16_f16(av, bq, acc, 0, 0, 0);
             else return __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, bq, acc, 0, 0, 0);
         };
-        // scores of tile t are complete: add the correction bias (correction tiles), or mask the
-        // keys a row does not see (exact tiles of partially visible blocks, causal masks)
-        auto scores_done = [&](int t, f32x16& s0, f32x16& s1) SOL_INLINE {
+        // scores of tile t are complete: returns the tile's exponent offset bo.  Correction
+        // tiles: every tile but the last holds 64 unselected full blocks (the ragged last key
+        // block, the largest index, and the padding slots can only be in the last tile), so
+        // their multiplicity is the offset log2(64) and their scores stay untouched; the last
+        // tile gets the per-slot bias after the loop.  Exact tiles: mask the keys a row does not
+        // see (partially visible blocks under a causal mask).
+        auto scores_done = [&](int t, int j, f32x16& s0, f32x16& s1) SOL_INLINE -> float {
             if constexpr (APX) {
-                bias_apx(code(t), s0, s1);
+                return t < T - 1 ? kLog2BlockK : 0.f;
             } else if constexpr (CAUSAL) {
-                const int j = code(t);
                 if (j >= nr) mask_causal(j, s0, s1);
             }
+            return 0.f;
         };
-        issue_k(0, 0);
-        issue_v(0, 0);
-        if (T > 1) issue_k(1, 1);
+        // row max of a finished score tile in log2 units, offset included
+        auto tile_max_l2 = [&](const f32x16& s0, const f32x16& s1, float bo) SOL_INLINE -> float {
+            const float m = tile_max(s0, s1) * cl;
+            if constexpr (APX) return m + bo;
+            else return m;
+        };
+        // Tile codes are read one step before their copies are issued, so that no list read
+        // sits between a barrier and the copies and operand reads after it: entering step t,
+        // cv = code(t+1) (its V goes out in step t) and ck = code(t+2) (its K goes out in step t).
+        const int c0 = code(0);
+        issue_k(c0, 0);
+        issue_v(c0, 0);
+        int cv = 0, ck = 0;
+        if (T > 1) {
+            cv = code(1);
+            issue_k(cv, 1);
+        }
+        if (T > 2) ck = code(2);
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
         f32x16 s0 = f32x16{}, s1 = f32x16{};
         qk(apx_tag, S0{}, qop, s0, s1);
-        scores_done(0, s0, s1);
-        float mx = tile_max(s0, s1);
+        float bo = scores_done(0, c0, s0, s1);   // offset of the tile whose scores are in s0/s1
+        float mx = tile_max_l2(s0, s1, bo);
         // iteration t with t & 1 == P: K of tile t+1 in stage P^1, V of tile t in stage P
         // D = 128: one pipelined iteration as 32 MFMA slots.  Slots 0-3 run QK^T of tile t+1
         // while the exponentials of P block 0 of tile t are formed; three blocks of 8 slots then
@@ -1142,28 +1184,32 @@ void routed_attn_kernel(AttnArgs a) {
         auto step_generic = [&](auto par_tag, int t) SOL_INLINE {
             constexpr int P = decltype(par_tag)::value;
             rescale(mx);
-            if (t + 2 < T) issue_k(t + 2, P);
-            issue_v(t + 1, P ^ 1);
+            if (t + 2 < T) issue_k(ck, P);
+            issue_v(cv, P ^ 1);
+            const int cn = t + 3 < T ? code(t + 3) : 0;
             f32x16 n0 = f32x16{}, n1 = f32x16{};
             qk(apx_tag, std::integral_constant<int, P ^ 1>{}, qop, n0, n1);
             f16x8 pb[4];
-            exps(s0, s1, pb);
+            exps(s0, s1, pb, bo);
             pv(apx_tag, par_tag, pb);
-            scores_done(t + 1, n0, n1);
-            mx = tile_max(n0, n1);
+            bo = scores_done(t + 1, cv, n0, n1);
+            mx = tile_max_l2(n0, n1, bo);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             s0 = n0;
             s1 = n1;
+            cv = ck;
+            ck = cn;
         };
         auto step_slots = [&](auto par_tag, int t) SOL_INLINE {
             constexpr int P = decltype(par_tag)::value;
             constexpr int KOFF = (P ^ 1) * L::STAGE;   // K of tile t+1
             constexpr int VOFF = P * L::STAGE;         // V of tile t
             rescale(mx);
-            if (t + 2 < T) issue_k(t + 2, P);
-            issue_v(t + 1, P ^ 1);
-            const float msub = m_run == kNegInf ? 0.f : m_run;
+            if (t + 2 < T) issue_k(ck, P);
+            issue_v(cv, P ^ 1);
+            const int cn = t + 3 < T ? code(t + 3) : 0;
+            const float msub = (m_run == kNegInf ? 0.f : m_run) - bo;
             const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
             f16x8 pb[4];
             auto exp_pair = [&](int kk, int q) SOL_INLINE {   // elements 2q, 2q+1 of P block kk
@@ -1205,28 +1251,30 @@ void routed_attn_kernel(AttnArgs a) {
             f32x16 n0 = f32x16{}, n1 = f32x16{};
             prefetch(0);
             prefetch(1);
-            int ck = 0, cv = 0;   // operands consumed so far
+            int uk = 0, uv = 0;   // operands consumed so far
 #pragma unroll
             for (int sl = 0; sl < 32; ++sl) {
                 prefetch(sl + 2);
                 const int id = index(sl);
                 if (kind(sl) == 0) {
-                    const KT av = kop[(ck++) & 3];
+                    const KT av = kop[(uk++) & 3];
                     if (id & 1) n1 = mfma_qk(av, qop[id >> 1], n1);
                     else n0 = mfma_qk(av, qop[id >> 1], n0);
                 } else {
-                    const f16x8 av = vop[(cv++) & 3];
+                    const f16x8 av = vop[(uv++) & 3];
                     o[id & 3] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, pb[id >> 2], o[id & 3], 0, 0, 0);
                 }
                 if (sl < 4) exp_pair(0, sl);
                 else if (sl < 28 && !((sl - 4) & 1)) exp_pair(((sl - 4) >> 3) + 1, ((sl - 4) & 7) >> 1);
             }
-            scores_done(t + 1, n0, n1);
-            mx = tile_max(n0, n1);
+            bo = scores_done(t + 1, cv, n0, n1);
+            mx = tile_max_l2(n0, n1, bo);
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             s0 = n0;
             s1 = n1;
+            cv = ck;
+            ck = cn;
         };
         auto step = [&](auto par_tag, int t) SOL_INLINE {
             if constexpr (D == 128) step_slots(par_tag, t);
@@ -1241,10 +1289,11 @@ void routed_attn_kernel(AttnArgs a) {
             step(S0{}, t);
             ++t;
         }
-        // last tile (t == T-1)
-        if constexpr (!APX) mask_tail(code(T - 1), s0, s1);
+        // last tile (t == T-1): its max is taken again here, after the bias or the tail mask
+        if constexpr (APX) bias_apx(code(T - 1), s0, s1);
+        else mask_tail(code(T - 1), s0, s1);
         f16x8 pb[4];
-        softmax(s0, s1, pb);
+        softmax(s0, s1, pb, bo);
         if ((T - 1) & 1) pv(apx_tag, S1{}, pb);
         else pv(apx_tag, S0{}, pb);
     };
