@@ -813,7 +813,9 @@ void routed_attn_kernel(AttnArgs a) {
     f32x16 o[NDT];
 #pragma unroll
     for (int mt = 0; mt < NDT; ++mt) o[mt] = f32x16{};
-    float m_run = kNegInf, l_run = 0.f;
+    // Row sum of the probabilities in four partial sums, one per 16-key block of a tile, so
+    // that the dot-product accumulations of a tile form four short dependency chains.
+    float m_run = kNegInf, l_run[4] = {0.f, 0.f, 0.f, 0.f};
 
     auto tile_code = [&](int n) -> int { return MODE == kDense ? n : (int)elist[n]; };
     // Global->LDS copies.  Each lane moves one 16-byte chunk per instruction; the per-lane
@@ -1036,17 +1038,24 @@ void routed_attn_kernel(AttnArgs a) {
     //               P.  bo is a per-tile exponent offset: log2(64) for correction tiles whose
     //               64 slots are all full routable blocks (their multiplicity), else 0.
     auto tile_max = [&](const f32x16& s0, const f32x16& s1) SOL_INLINE -> float {
-        // balanced tree over the lane's 32 scores (short dependency chains) ...
-        float m[16];
+        // balanced tree of three-input maxima over the lane's 32 scores (v_max3: 17 instructions,
+        // short dependency chains) ...
+        float x[32];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) m[r] = fmaxf(s0[r], s1[r]);
+        for (int r = 0; r < 16; ++r) {
+            x[r] = s0[r];
+            x[16 + r] = s1[r];
+        }
+        float a3[11];
 #pragma unroll
-        for (int w = 8; w > 0; w >>= 1)
-#pragma unroll
-            for (int r = 0; r < w; ++r) m[r] = fmaxf(m[r], m[r + w]);
+        for (int i = 0; i < 10; ++i) a3[i] = fmaxf(fmaxf(x[3 * i], x[3 * i + 1]), x[3 * i + 2]);
+        a3[10] = fmaxf(x[30], x[31]);
+        const float b0 = fmaxf(fmaxf(a3[0], a3[1]), a3[2]), b1 = fmaxf(fmaxf(a3[3], a3[4]), a3[5]);
+        const float b2 = fmaxf(fmaxf(a3[6], a3[7]), a3[8]), b3 = fmaxf(a3[9], a3[10]);
+        const float m0 = fmaxf(fmaxf(fmaxf(b0, b1), b2), b3);
         // ... then across the lane pair (l, l+32) that holds the query's other 32 keys, with a
         // VALU lane swap instead of an LDS permute
-        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(m[0]), __float_as_uint(m[0]), false, false);
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(m0), __float_as_uint(m0), false, false);
         return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
     };
     auto rescale = [&](float mt_) SOL_INLINE {
@@ -1056,7 +1065,8 @@ void routed_attn_kernel(AttnArgs a) {
             const float alpha = (m_run == kNegInf) ? 0.f : __builtin_amdgcn_exp2f(m_run - mnew);
 #pragma unroll
             for (int mt = 0; mt < NDT; ++mt) o[mt] *= alpha;
-            l_run *= alpha;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) l_run[u] *= alpha;
             m_run = mnew;
         }
     };
@@ -1075,7 +1085,7 @@ void routed_attn_kernel(AttnArgs a) {
                     const float p0 = __builtin_amdgcn_exp2f(fmaf(x0, cl, -msub));
                     const float p1 = __builtin_amdgcn_exp2f(fmaf(x1, cl, -msub));
                     const f16x2 pp = {(_Float16)p0, (_Float16)p1};
-                    l_run = __builtin_amdgcn_fdot2(pp, ones, l_run, false);
+                    l_run[2 * tt + sh] = __builtin_amdgcn_fdot2(pp, ones, l_run[2 * tt + sh], false);
                     pb[2 * tt + sh][e] = pp[0];
                     pb[2 * tt + sh][e + 1] = pp[1];
                 }
@@ -1175,11 +1185,12 @@ void routed_attn_kernel(AttnArgs a) {
         float bo = scores_done(0, c0, s0, s1);   // offset of the tile whose scores are in s0/s1
         float mx = tile_max_l2(s0, s1, bo);
         // iteration t with t & 1 == P: K of tile t+1 in stage P^1, V of tile t in stage P
-        // D = 128: one pipelined iteration as 32 MFMA slots.  Slots 0-3 run QK^T of tile t+1
-        // while the exponentials of P block 0 of tile t are formed; three blocks of 8 slots then
-        // alternate QK^T(t+1) and PV(t) while the next P block is formed; the last 4 slots are
-        // PV only, overlapped with the row max of tile t+1.  Successive MFMAs on one accumulator
-        // are at least two slots apart, and operands are read from LDS two slots ahead.
+        // D = 128: one pipelined iteration as 32 MFMA slots.  Slots 0-15 run QK^T of tile t+1
+        // while the exponentials of tile t are formed (one pair per slot, P block k in slots
+        // 4k..4k+3); slots 16-31 run PV of tile t, which leaves their 16 MFMAs to hide the row
+        // max of tile t+1 (finishing QK^T(t+1) early measured 1-2% faster than interleaving it
+        // with PV(t)).  Successive MFMAs on one accumulator are at least two slots apart, and
+        // operands are read from LDS two slots ahead.
         // Generic iteration (any D): the same work in source order.
         auto step_generic = [&](auto par_tag, int t) SOL_INLINE {
             constexpr int P = decltype(par_tag)::value;
@@ -1219,20 +1230,14 @@ void routed_attn_kernel(AttnArgs a) {
                 const float p0 = __builtin_amdgcn_exp2f(fmaf(x0, cl, -msub));
                 const float p1 = __builtin_amdgcn_exp2f(fmaf(x1, cl, -msub));
                 const f16x2 pp = {(_Float16)p0, (_Float16)p1};
-                l_run = __builtin_amdgcn_fdot2(pp, ones, l_run, false);
+                l_run[kk] = __builtin_amdgcn_fdot2(pp, ones, l_run[kk], false);
                 pb[kk][2 * q] = pp[0];
                 pb[kk][2 * q + 1] = pp[1];
             };
-            // slot -> operation: kind 0 = QK (index qi: ks = qi/2, half = qi%2), 1 = PV (pi: kk = pi/4)
-            auto kind = [](int sl) SOL_INLINE { return sl < 4 ? 0 : (sl < 28 ? ((sl - 4) & 1) : 1); };
-            auto index = [](int sl) SOL_INLINE {
-                if (sl < 4) return sl;
-                if (sl < 28) {
-                    const int u = sl - 4, b = u >> 3, w = u & 7;
-                    return (w & 1) ? 4 * b + (w >> 1) : 4 + 4 * b + (w >> 1);
-                }
-                return 12 + (sl - 28);
-            };
+            // slot -> operation: slots 0-15 QK^T (index i: k-step i/2, key half i%2), slots 16-31
+            // PV (index i: k-step i/4, d M-tile i%4)
+            auto kind = [](int sl) SOL_INLINE { return sl < 16 ? 0 : 1; };
+            auto index = [](int sl) SOL_INLINE { return sl < 16 ? sl : sl - 16; };
             auto ldk = [&](int qi) SOL_INLINE {
                 return *reinterpret_cast<const KT*>(smem + kadr[qi >> 1] + KOFF + (qi & 1) * KT1);
             };
@@ -1264,8 +1269,7 @@ void routed_attn_kernel(AttnArgs a) {
                     const f16x8 av = vop[(uv++) & 3];
                     o[id & 3] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, pb[id >> 2], o[id & 3], 0, 0, 0);
                 }
-                if (sl < 4) exp_pair(0, sl);
-                else if (sl < 28 && !((sl - 4) & 1)) exp_pair(((sl - 4) >> 3) + 1, ((sl - 4) & 7) >> 1);
+                if (sl < 16) exp_pair(sl >> 2, sl & 3);
             }
             bo = scores_done(t + 1, cv, n0, n1);
             mx = tile_max_l2(n0, n1, bo);
@@ -1319,7 +1323,8 @@ void routed_attn_kernel(AttnArgs a) {
     }
 
     // ---- epilogue: O = O^T / l, bf16
-    const float lt = l_run + __shfl_xor(l_run, 32);
+    const float lsum = (l_run[0] + l_run[1]) + (l_run[2] + l_run[3]);
+    const float lt = lsum + __shfl_xor(lsum, 32);
     const float inv = lt > 0.f ? 1.0f / lt : 0.f;
     if (qrow < a.N) {
         uint16_t* op = a.out + ((size_t)bh * a.N + qrow) * D;
