@@ -34,9 +34,9 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_24027_amd", "csrc", "sol_attn_ker
 # then WRITE_SIZE), each scaled by what the same counter reads for the 1 GiB calibration copy
 # (FETCH x 2.000, WRITE x 1.000).  Valid only for the kernel source and workload it was taken on.
 MEASURED_TRAFFIC = {
-    "kernel_sha256": "5e4f5542fcc5dc80d79b56a30d18692d5c13321b6c206c36853bd44d3bbe38fd",
+    "kernel_sha256": "016a3fe2e52f397dcd752293326f18351df42952759ea475fa7366968878529b",
     "workload": "video720p", "kept": 0.2,
-    "fetch_bytes": 144.83e9, "write_bytes": 0.7755e9,
+    "fetch_bytes": 105.22e9, "write_bytes": 0.7759e9,
 }
 
 
@@ -241,7 +241,7 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": MFMA_BF16_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": r4(achieved / MFMA_BF16_PEAK_TFLOPS),
                      "traffic": measured_traffic(w.name, kept),
-                     "kernel": "routed_attn_kernel<128,128,sparse>",
+                     "kernel": f"routed_attn_kernel<{w.d},{w.block_q},sparse>",
                      "flop_per_launch": exact_flop + approx_flop, "exact_flop": exact_flop,
                      "correction_flop": approx_flop},
     }

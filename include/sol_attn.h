@@ -159,7 +159,10 @@ int sol_attn_forward(const void* q, const void* k, const void* v, void* out,
  * stream: hipStream_t or NULL.
  *
  * Selection is computed on chip from f32 pooled proxies s*Qbar_i.Kbar_j and
- * never written to memory unless mask_out is given.
+ * never written to memory unless mask_out is given.  In the sparse modes the
+ * library also orders the query blocks of each head by their pooled queries, so
+ * that blocks with similar selections run together and share L2; this changes
+ * only which workgroup computes which block, never a result.
  */
 int sol_attn_forward_ex(const void* q, const void* k, const void* v, void* out,
                         int B, int H, int N, int d, int block_q, int block_k,

@@ -42,6 +42,8 @@ struct Workspace {
     float* muk = nullptr;        // [BH][d]
     float* cov = nullptr;        // [BH][d][d]
     float* tau = nullptr;        // [BH][NQ]
+    float* sigma = nullptr;      // [BH][NQ] sigma_i of the thresholds (query-block order)
+    uint16_t* order = nullptr;   // [BH][NQ] query-block order of the sparse kernels
     double* mom = nullptr;       // partial moments, moments_scratch_bytes()
     uint32_t* blkcount = nullptr;// [BH][NQ]
 };

@@ -473,6 +473,205 @@ __device__ int block_scan_incl(int v, int* scratch, int* total) {
     return v + pre;
 }
 
+// ---------------------------------------------------------------------------
+// Query-block order of the sparse kernels (scheduling only).
+// The workgroups resident on one XCD share its L2, and a key block's tiles are served from L2
+// only if the workgroups that select it read them close together in time.  Whether two query
+// blocks select alike depends on their pooled queries as seen by the pooled keys: row i keeps
+// key block j iff Qbar_i (Kbar_j - mu_K) exceeds beta sigma_i / s, so only the direction of
+// Qbar_i in the space the pooled keys span matters.  The blocks of each head are therefore
+// ordered along a Hilbert curve over (Qbar_i u1, Qbar_i u2) / sigma_i, with u1 and u2 the two
+// leading eigenvectors of C_K (power iteration from fixed start vectors), and the sparse kernel
+// hands consecutive blocks of that order to the same XCD.  Each query block is still computed
+// by one workgroup exactly as in the identity order: the order decides which blocks run
+// together, never a result.  Heads with more than kOrderMaxNQ query blocks keep the identity.
+// ---------------------------------------------------------------------------
+constexpr int kOrderMaxNQ = 4096;
+constexpr int kOrderGrid = 256;   // Hilbert curve over a 256 x 256 grid: 16-bit indices
+
+__device__ __forceinline__ uint32_t hilbert_index(uint32_t x, uint32_t y) {
+    uint32_t d = 0;
+    for (uint32_t s = kOrderGrid / 2; s > 0; s >>= 1) {
+        const uint32_t rx = (x & s) ? 1u : 0u, ry = (y & s) ? 1u : 0u;
+        d += s * s * ((3u * rx) ^ ry);
+        if (ry == 0u) {   // rotate the quadrant
+            if (rx == 1u) {
+                x = kOrderGrid - 1 - x;
+                y = kOrderGrid - 1 - y;
+            }
+            const uint32_t tmp = x;
+            x = y;
+            y = tmp;
+        }
+    }
+    return d;
+}
+
+template <int NT>
+__device__ float block_max(float v, float* scratch) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
+    if (lane == 0) scratch[wave] = v;
+    __syncthreads();
+    float m = scratch[0];
+#pragma unroll
+    for (int w = 1; w < NT / 64; ++w) m = fmaxf(m, scratch[w]);
+    __syncthreads();
+    return m;
+}
+
+template <int NT>
+__device__ float2 block_sum2(float x, float y, float2* scratch) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        x += __shfl_xor(x, off);
+        y += __shfl_xor(y, off);
+    }
+    if (lane == 0) scratch[wave] = make_float2(x, y);
+    __syncthreads();
+    float2 tot = make_float2(0.f, 0.f);
+#pragma unroll
+    for (int w = 0; w < NT / 64; ++w) {
+        tot.x += scratch[w].x;
+        tot.y += scratch[w].y;
+    }
+    __syncthreads();
+    return tot;
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void order_kernel(const float* __restrict__ qbar, const float* __restrict__ cov,
+                                                    const float* __restrict__ sigma, uint16_t* __restrict__ order,
+                                                    int NQ) {
+    constexpr int NT = 256;
+    constexpr int ITERS = 12;        // power iterations per eigenvector (only an ordering depends on them)
+    constexpr int EPL = D / 64;      // elements of a D-vector per lane
+    __shared__ float u[2][D];
+    __shared__ float vb[D];
+    __shared__ float scratch[NT / 64];
+    __shared__ float2 scratch2[NT / 64];
+    __shared__ float pa[kOrderMaxNQ], pb[kOrderMaxNQ];
+    __shared__ uint32_t keys[kOrderMaxNQ];
+    const int bh = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    uint16_t* ord = order + (size_t)bh * NQ;
+    if (NQ > kOrderMaxNQ) {
+        for (int i = t; i < NQ; i += NT) ord[i] = (uint16_t)i;
+        return;
+    }
+    // power iteration: u1, then u2 kept orthogonal to u1.  C_K is symmetric, so thread r < D
+    // holds column r (= row r) in registers and forms (C v)_r from the vector in LDS.
+    float ccol[D];
+    if (t < D) {
+#pragma unroll
+        for (int c = 0; c < D; ++c) ccol[c] = cov[((size_t)bh * D + c) * D + t];
+    }
+    for (int e = 0; e < 2; ++e) {
+        if (t < D) vb[t] = (float)((((uint32_t)t + 1u + 977u * (uint32_t)e) * 2654435761u) >> 22) / 1024.f - 0.5f;
+        __syncthreads();
+        for (int it = 0; it < ITERS; ++it) {
+            float w = 0.f;
+            if (t < D) {
+                float w4[4] = {0.f, 0.f, 0.f, 0.f};   // four short chains
+#pragma unroll
+                for (int c = 0; c < D; ++c) w4[c & 3] = fmaf(ccol[c], vb[c], w4[c & 3]);
+                w = (w4[0] + w4[1]) + (w4[2] + w4[3]);
+            }
+            // one reduction for |w|^2 and u1.w: |w - (u1.w) u1|^2 = |w|^2 - (u1.w)^2 for unit u1
+            const float2 r = block_sum2<NT>(t < D ? w * w : 0.f, (t < D && e == 1) ? w * u[0][t] : 0.f, scratch2);
+            if (e == 1 && t < D) w -= r.y * u[0][t];
+            const float nrm = sqrtf(fmaxf(r.x - (e == 1 ? r.y * r.y : 0.f), 0.f));
+            if (t < D) vb[t] = nrm > 0.f ? w / nrm : 0.f;
+            __syncthreads();
+        }
+        if (t < D) u[e][t] = vb[t];
+        __syncthreads();
+    }
+    // projections (Qbar_i u1, Qbar_i u2) / sigma_i: one wave per row, coalesced
+    float ua[EPL], ub[EPL];
+#pragma unroll
+    for (int r = 0; r < EPL; ++r) {
+        ua[r] = u[0][lane + 64 * r];
+        ub[r] = u[1][lane + 64 * r];
+    }
+    constexpr int RB = 16;   // rows per wave and batch: their loads are in flight together
+    for (int i0 = wave * RB; i0 < NQ; i0 += RB * (NT / 64)) {
+        float qv[RB][EPL];
+#pragma unroll
+        for (int rr = 0; rr < RB; ++rr) {
+            const float* qr = qbar + ((size_t)bh * NQ + min(i0 + rr, NQ - 1)) * D;
+#pragma unroll
+            for (int r = 0; r < EPL; ++r) qv[rr][r] = qr[lane + 64 * r];
+        }
+#pragma unroll
+        for (int rr = 0; rr < RB; ++rr) {
+            float a0 = 0.f, b0 = 0.f;
+#pragma unroll
+            for (int r = 0; r < EPL; ++r) {
+                a0 = fmaf(qv[rr][r], ua[r], a0);
+                b0 = fmaf(qv[rr][r], ub[r], b0);
+            }
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) {
+                a0 += __shfl_xor(a0, off);
+                b0 += __shfl_xor(b0, off);
+            }
+            const int i = i0 + rr;
+            if (lane == 0 && i < NQ) {
+                const float sg = sigma[(size_t)bh * NQ + i];
+                const float inv = sg > 0.f ? 1.f / sg : 1.f;
+                pa[i] = a0 * inv;
+                pb[i] = b0 * inv;
+            }
+        }
+    }
+    __syncthreads();
+    float amax = -__builtin_huge_valf(), amin_n = -__builtin_huge_valf();
+    float bmax = -__builtin_huge_valf(), bmin_n = -__builtin_huge_valf();
+    for (int i = t; i < NQ; i += NT) {
+        amax = fmaxf(amax, pa[i]);
+        amin_n = fmaxf(amin_n, -pa[i]);
+        bmax = fmaxf(bmax, pb[i]);
+        bmin_n = fmaxf(bmin_n, -pb[i]);
+    }
+    amax = block_max<NT>(amax, scratch);
+    const float amin = -block_max<NT>(amin_n, scratch);
+    bmax = block_max<NT>(bmax, scratch);
+    const float bmin = -block_max<NT>(bmin_n, scratch);
+    const float ascl = amax > amin ? (float)(kOrderGrid - 1) / (amax - amin) : 0.f;
+    const float bscl = bmax > bmin ? (float)(kOrderGrid - 1) / (bmax - bmin) : 0.f;
+    int P = 1;
+    while (P < NQ) P <<= 1;
+    for (int i = t; i < P; i += NT) {
+        uint32_t key = 0xffffffffu;
+        if (i < NQ) {
+            const uint32_t gx = (uint32_t)min(kOrderGrid - 1, max(0, (int)((pa[i] - amin) * ascl + 0.5f)));
+            const uint32_t gy = (uint32_t)min(kOrderGrid - 1, max(0, (int)((pb[i] - bmin) * bscl + 0.5f)));
+            key = (hilbert_index(gx, gy) << 16) | (uint32_t)i;
+        }
+        keys[i] = key;
+    }
+    __syncthreads();
+    // bitonic sort, ascending; keys are distinct (the block index is in the low bits)
+    for (int k = 2; k <= P; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = t; i < P; i += NT) {
+                const int l = i ^ j;
+                if (l > i) {
+                    const uint32_t x = keys[i], y = keys[l];
+                    if ((x > y) == ((i & k) == 0)) {
+                        keys[i] = y;
+                        keys[l] = x;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+    for (int i = t; i < NQ; i += NT) ord[i] = (uint16_t)(keys[i] & 0xffffu);
+}
+
 template <int D, int NT, int MODE, bool CAUSAL = false>
 __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __restrict__ kbar_h, float tau_i,
                               float beta, float scale, int NKr, int nr, int ne, int MW, float* prox, uint32_t* selw,
@@ -642,6 +841,7 @@ struct AttnArgs {
     uint16_t* out;
     uint32_t* blkcount;
     uint32_t* mask_out;
+    const uint16_t* order;        // [BH][NQ] query-block order (sparse modes), or null: identity
     int BH, N, NQ, NK, NKr, NC, MW, per_x;
     float scale, c_log2;
     float bias_full, bias_last;   // log2(n_j)/c_log2 for full blocks and for the last block
@@ -772,6 +972,7 @@ void routed_attn_kernel(AttnArgs a) {
         qi = u < hp ? (15 - xcd) * hp + (hp - 1 - u) : xcd * hp + (u - hp);
     } else {
         qi = xcd * a.per_x + (y % a.per_x);
+        if (a.order != nullptr && bh < a.BH && qi < a.NQ) qi = a.order[(size_t)bh * a.NQ + qi];
     }
     if (bh >= a.BH || qi >= a.NQ) return;
 
@@ -1586,6 +1787,8 @@ size_t workspace_layout(const Shape& s, char* base, Workspace* ws) {
         w.muk = reinterpret_cast<float*>(take(BH * d * 4));
         w.cov = reinterpret_cast<float*>(take(BH * d * d * 4));
         w.tau = reinterpret_cast<float*>(take(BH * s.NQ * 4));
+        w.sigma = reinterpret_cast<float*>(take(BH * s.NQ * 4));
+        w.order = reinterpret_cast<uint16_t*>(take(BH * s.NQ * 2));
         w.mom = reinterpret_cast<double*>(take(moments_scratch_bytes(s.BH, s.d)));
     }
     if (s.dtype == kBF16) {
@@ -1668,12 +1871,16 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
             if (!s.causal) {   // causal masks: the kernel takes each row's statistics itself
                 if ((e = launch_moments(ws.kbar, ws.muk, ws.cov, ws.mom, s.BH, s.NK, s.NKr, d, st)) != hipSuccess)
                     return e;
-                if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, nullptr, s.BH, s.NQ, d, beta, s.diag,
+                if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, ws.sigma, s.BH, s.NQ, d, beta, s.diag,
                                     st)) != hipSuccess)
                     return e;
+                if (d == 128) order_kernel<128><<<dim3(s.BH), dim3(256), 0, st>>>(ws.qbar, ws.cov, ws.sigma, ws.order, s.NQ);
+                else order_kernel<64><<<dim3(s.BH), dim3(256), 0, st>>>(ws.qbar, ws.cov, ws.sigma, ws.order, s.NQ);
+                if ((e = hipGetLastError()) != hipSuccess) return e;
             }
         }
         AttnArgs a{};
+        a.order = (routing && !s.causal) ? ws.order : nullptr;
         a.q = static_cast<const uint16_t*>(q);
         a.k = kk;
         a.vt = ws.vt;
