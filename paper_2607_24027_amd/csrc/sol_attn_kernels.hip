@@ -508,20 +508,6 @@ __device__ __forceinline__ uint32_t hilbert_index(uint32_t x, uint32_t y) {
 }
 
 template <int NT>
-__device__ float block_max(float v, float* scratch) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
-    if (lane == 0) scratch[wave] = v;
-    __syncthreads();
-    float m = scratch[0];
-#pragma unroll
-    for (int w = 1; w < NT / 64; ++w) m = fmaxf(m, scratch[w]);
-    __syncthreads();
-    return m;
-}
-
-template <int NT>
 __device__ float2 block_sum2(float x, float y, float2* scratch) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
@@ -546,14 +532,14 @@ __global__ __launch_bounds__(256) void order_kernel(const float* __restrict__ qb
                                                     const float* __restrict__ sigma, uint16_t* __restrict__ order,
                                                     int NQ) {
     constexpr int NT = 256;
-    constexpr int ITERS = 12;        // power iterations per eigenvector (only an ordering depends on them)
-    constexpr int EPL = D / 64;      // elements of a D-vector per lane
+    constexpr int ITERS = 4;         // power iterations per eigenvector: an offline study of the synthetic
+                                     // workloads found the order as good as with 12
     __shared__ float u[2][D];
     __shared__ float vb[D];
-    __shared__ float scratch[NT / 64];
     __shared__ float2 scratch2[NT / 64];
+    __shared__ float red4[NT / 64][4];
     __shared__ float pa[kOrderMaxNQ], pb[kOrderMaxNQ];
-    __shared__ uint32_t keys[kOrderMaxNQ];
+    __shared__ __attribute__((aligned(16))) uint32_t keys[kOrderMaxNQ];
     const int bh = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
     uint16_t* ord = order + (size_t)bh * NQ;
     if (NQ > kOrderMaxNQ) {
@@ -588,88 +574,84 @@ __global__ __launch_bounds__(256) void order_kernel(const float* __restrict__ qb
         if (t < D) u[e][t] = vb[t];
         __syncthreads();
     }
-    // projections (Qbar_i u1, Qbar_i u2) / sigma_i: one wave per row, coalesced
-    float ua[EPL], ub[EPL];
+    // projections (Qbar_i u1, Qbar_i u2) / sigma_i, one thread per row (16-byte row reads, no
+    // cross-lane reductions); u1 and u2 are broadcast from LDS
+    for (int i = t; i < NQ; i += NT) {
+        const f32x4* qr = reinterpret_cast<const f32x4*>(qbar + ((size_t)bh * NQ + i) * D);
+        float a4[4] = {0.f, 0.f, 0.f, 0.f}, b4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int r = 0; r < EPL; ++r) {
-        ua[r] = u[0][lane + 64 * r];
-        ub[r] = u[1][lane + 64 * r];
-    }
-    constexpr int RB = 16;   // rows per wave and batch: their loads are in flight together
-    for (int i0 = wave * RB; i0 < NQ; i0 += RB * (NT / 64)) {
-        float qv[RB][EPL];
+        for (int c4 = 0; c4 < D / 4; ++c4) {
+            const f32x4 qv = qr[c4];
 #pragma unroll
-        for (int rr = 0; rr < RB; ++rr) {
-            const float* qr = qbar + ((size_t)bh * NQ + min(i0 + rr, NQ - 1)) * D;
-#pragma unroll
-            for (int r = 0; r < EPL; ++r) qv[rr][r] = qr[lane + 64 * r];
-        }
-#pragma unroll
-        for (int rr = 0; rr < RB; ++rr) {
-            float a0 = 0.f, b0 = 0.f;
-#pragma unroll
-            for (int r = 0; r < EPL; ++r) {
-                a0 = fmaf(qv[rr][r], ua[r], a0);
-                b0 = fmaf(qv[rr][r], ub[r], b0);
-            }
-#pragma unroll
-            for (int off = 32; off > 0; off >>= 1) {
-                a0 += __shfl_xor(a0, off);
-                b0 += __shfl_xor(b0, off);
-            }
-            const int i = i0 + rr;
-            if (lane == 0 && i < NQ) {
-                const float sg = sigma[(size_t)bh * NQ + i];
-                const float inv = sg > 0.f ? 1.f / sg : 1.f;
-                pa[i] = a0 * inv;
-                pb[i] = b0 * inv;
+            for (int e = 0; e < 4; ++e) {
+                a4[e] = fmaf(qv[e], u[0][4 * c4 + e], a4[e]);
+                b4[e] = fmaf(qv[e], u[1][4 * c4 + e], b4[e]);
             }
         }
+        const float sg = sigma[(size_t)bh * NQ + i];
+        const float inv = sg > 0.f ? 1.f / sg : 1.f;
+        pa[i] = ((a4[0] + a4[1]) + (a4[2] + a4[3])) * inv;
+        pb[i] = ((b4[0] + b4[1]) + (b4[2] + b4[3])) * inv;
     }
     __syncthreads();
-    float amax = -__builtin_huge_valf(), amin_n = -__builtin_huge_valf();
-    float bmax = -__builtin_huge_valf(), bmin_n = -__builtin_huge_valf();
+    // bounding box of the projections: one reduction of four maxima
+    float m4[4] = {-__builtin_huge_valf(), -__builtin_huge_valf(), -__builtin_huge_valf(), -__builtin_huge_valf()};
     for (int i = t; i < NQ; i += NT) {
-        amax = fmaxf(amax, pa[i]);
-        amin_n = fmaxf(amin_n, -pa[i]);
-        bmax = fmaxf(bmax, pb[i]);
-        bmin_n = fmaxf(bmin_n, -pb[i]);
+        m4[0] = fmaxf(m4[0], pa[i]);
+        m4[1] = fmaxf(m4[1], -pa[i]);
+        m4[2] = fmaxf(m4[2], pb[i]);
+        m4[3] = fmaxf(m4[3], -pb[i]);
     }
-    amax = block_max<NT>(amax, scratch);
-    const float amin = -block_max<NT>(amin_n, scratch);
-    bmax = block_max<NT>(bmax, scratch);
-    const float bmin = -block_max<NT>(bmin_n, scratch);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) m4[q] = fmaxf(m4[q], __shfl_xor(m4[q], off));
+    }
+    if (lane == 0)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) red4[wave][q] = m4[q];
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        m4[q] = red4[0][q];
+#pragma unroll
+        for (int w = 1; w < NT / 64; ++w) m4[q] = fmaxf(m4[q], red4[w][q]);
+    }
+    const float amax = m4[0], amin = -m4[1], bmax = m4[2], bmin = -m4[3];
     const float ascl = amax > amin ? (float)(kOrderGrid - 1) / (amax - amin) : 0.f;
     const float bscl = bmax > bmin ? (float)(kOrderGrid - 1) / (bmax - bmin) : 0.f;
-    int P = 1;
-    while (P < NQ) P <<= 1;
-    for (int i = t; i < P; i += NT) {
-        uint32_t key = 0xffffffffu;
-        if (i < NQ) {
-            const uint32_t gx = (uint32_t)min(kOrderGrid - 1, max(0, (int)((pa[i] - amin) * ascl + 0.5f)));
-            const uint32_t gy = (uint32_t)min(kOrderGrid - 1, max(0, (int)((pb[i] - bmin) * bscl + 0.5f)));
-            key = (hilbert_index(gx, gy) << 16) | (uint32_t)i;
-        }
-        keys[i] = key;
+    for (int i = t; i < NQ; i += NT) {
+        const uint32_t gx = (uint32_t)min(kOrderGrid - 1, max(0, (int)((pa[i] - amin) * ascl + 0.5f)));
+        const uint32_t gy = (uint32_t)min(kOrderGrid - 1, max(0, (int)((pb[i] - bmin) * bscl + 0.5f)));
+        keys[i] = (hilbert_index(gx, gy) << 16) | (uint32_t)i;   // distinct: the block index is in the low bits
     }
+    for (int i = NQ + t; i < ((NQ + 3) & ~3); i += NT) keys[i] = 0xffffffffu;   // pad to whole 16-byte reads
     __syncthreads();
-    // bitonic sort, ascending; keys are distinct (the block index is in the low bits)
-    for (int k = 2; k <= P; k <<= 1) {
-        for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = t; i < P; i += NT) {
-                const int l = i ^ j;
-                if (l > i) {
-                    const uint32_t x = keys[i], y = keys[l];
-                    if ((x > y) == ((i & k) == 0)) {
-                        keys[i] = y;
-                        keys[l] = x;
-                    }
-                }
-            }
-            __syncthreads();
+    // rank sort: block i goes to position |{j : key_j < key_i}|.  Each thread ranks all of its
+    // keys (at most KPT) in one pass over the keys, read four at a time.
+    constexpr int KPT = kOrderMaxNQ / NT;
+    uint32_t mine[KPT];
+    int rank[KPT];
+#pragma unroll
+    for (int r = 0; r < KPT; ++r) {
+        const int i = t + NT * r;
+        mine[r] = i < NQ ? keys[i] : 0u;
+        rank[r] = 0;
+    }
+    const int nmine = (NQ - t + NT - 1) / NT;   // keys this thread owns (wave-divergent only at the edge)
+    const uint4* k4 = reinterpret_cast<const uint4*>(keys);
+    for (int j4 = 0; j4 < (NQ + 3) / 4; ++j4) {
+        const uint4 kj = k4[j4];
+#pragma unroll
+        for (int r = 0; r < KPT; ++r) {
+            if (r < nmine)
+                rank[r] += (kj.x < mine[r] ? 1 : 0) + (kj.y < mine[r] ? 1 : 0) + (kj.z < mine[r] ? 1 : 0) +
+                           (kj.w < mine[r] ? 1 : 0);
         }
     }
-    for (int i = t; i < NQ; i += NT) ord[i] = (uint16_t)(keys[i] & 0xffffu);
+#pragma unroll
+    for (int r = 0; r < KPT; ++r)
+        if (r < nmine) ord[rank[r]] = (uint16_t)(t + NT * r);
 }
 
 template <int D, int NT, int MODE, bool CAUSAL = false>
