@@ -7,6 +7,8 @@
 //   3. moments        mean and centred covariance of the routable pooled keys, f64 sums
 //   4. tau            tau_i = mu_i + beta*sigma_i from the moments   (Eqs. threshold_routing,
 //                                                                       threshold_stats_exact)
+//   4b. order         sparse modes: order of each head's query blocks for the attention
+//                     grid (scheduling only: blocks with similar selections share an L2)
 //   5. routed_attn    one workgroup per (b, h, query block): routes every key block on chip
 //                     from f32 proxies, then runs one online-softmax pass over correction
 //                     tiles (pooled keys, Section 3.2 "Proxy-Score Reuse") and exact tiles
