@@ -136,6 +136,27 @@ def test_forward_parity_edge_shapes(dev, name, mode, beta):
     assert_output_close(to_np(out), ref["out"], w.dtype, f"edge {name}/{mode}/{beta}")
 
 
+@pytest.mark.parametrize("nq", [4096, 4100])
+def test_query_block_order_limits(dev, nq):
+    # The sparse kernels take the query blocks of each head in an order computed on the GPU
+    # for up to 4096 blocks per head (every rank-sort slot of a thread in use at 4096) and in
+    # the identity order above that.  d = 64, block_q = 64: N = 64 * nq tokens, one head;
+    # complete mask, sampled query blocks, every output row written.
+    w = small_workload(f"order{nq}", (nq, 64), 64, 64, H=1)
+    q, k, v = synth.make_qkv(w)
+    print(f"[parity] query-block order limit NQ={nq} N={w.N}", flush=True)
+    r = ora.routing(to_np(q), to_np(k), w.block_q, 64, 0.8)
+    for mode in ("sparse", "sparse_no_correction"):
+        out, gmask, counts = run_gpu(dev, w, q, k, v, 0.8, mode)
+        assert_mask_matches(gmask, r["mask"], r["s_hat"], r["tau"])
+        assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
+        qblocks = [0, 1, nq // 3, nq // 2, nq - 1]
+        ref = ora.forward(to_np(q), to_np(k), to_np(v), w.block_q, 64, 0.8, mode, query_blocks=qblocks, mask=gmask)
+        rows = np.concatenate([np.arange(i * w.block_q, min((i + 1) * w.block_q, w.N)) for i in qblocks])
+        got = out.float().cpu().numpy().astype(np.float64)
+        assert_output_close(got[:, :, rows], ref["out"][:, :, rows], w.dtype, f"order{nq}/{mode}")
+
+
 @pytest.mark.parametrize("name", ["bf16_d128_q128", "f32_d64_q64"])
 @pytest.mark.parametrize("beta", [0.8, -0.5, -INF, INF])
 def test_thresholds_parity(dev, name, beta):
