@@ -136,6 +136,50 @@ def test_forward_parity_edge_shapes(dev, name, mode, beta):
     assert_output_close(to_np(out), ref["out"], w.dtype, f"edge {name}/{mode}/{beta}")
 
 
+def random_case(seed):
+    """A seeded random forward configuration: shape, block sizes, dtype, text tail, cutoff, mode."""
+    rng = np.random.default_rng(1000 + seed)
+    d = int(rng.choice([64, 128]))
+    bq = int(rng.choice([64, 128]))
+    dtype = "f32" if rng.random() < 0.2 else "bf16"
+    n_img = int(rng.integers(1, 6000))
+    shape = int(rng.integers(1, 4))                       # 1D, 2D or 3D token grid
+    if shape == 1:
+        grid = (n_img,)
+    elif shape == 2:
+        a = int(rng.integers(1, 80))
+        grid = (a, max(1, n_img // a))
+    else:
+        a, b = int(rng.integers(1, 12)), int(rng.integers(1, 30))
+        grid = (a, b, max(1, n_img // (a * b)))
+    text = 64 * int(rng.integers(1, 9)) if (dtype == "bf16" and rng.random() < 0.3) else 0
+    B, H = int(rng.integers(1, 3)), int(rng.integers(1, 4))
+    r = rng.random()
+    beta = -INF if r < 0.1 else (INF if r < 0.2 else float(np.round(rng.uniform(-1.0, 2.0), 3)))
+    mode = str(rng.choice(["dense", "sparse", "sparse_no_correction"]))
+    return grid, d, bq, dtype, text, B, H, beta, mode
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_forward_parity_random_shapes(dev, seed):
+    # Seeded random configurations (any token count, ragged tails, 1D/2D/3D grids, text tails,
+    # both dtypes and block heights, cutoffs from -inf to +inf), element by element.
+    grid, d, bq, dtype, text, B, H, beta, mode = random_case(seed)
+    w = small_workload(f"rand{seed}", grid, d, bq, dtype=dtype, text_tokens=text, H=H, B=B, seed=50 + seed)
+    print(f"[parity] random {seed}: grid={grid} N={w.N} d={d} bq={bq} {dtype} text={text} B={B} H={H} "
+          f"beta={beta} {mode}", flush=True)
+    q, k, v = synth.make_qkv(w)
+    out, gmask, counts = run_gpu(dev, w, q, k, v, beta, mode)
+    qn, kn, vn = to_np(q), to_np(k), to_np(v)
+    ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens)
+    if mode != "dense":
+        flips = assert_mask_matches(gmask, ref["mask"], ref["s_hat"], ref["tau"])
+        if flips:
+            ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens, mask=gmask)
+        assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
+    assert_output_close(to_np(out), ref["out"], w.dtype, f"random {seed}")
+
+
 @pytest.mark.parametrize("nq", [4096, 4100])
 def test_query_block_order_limits(dev, nq):
     # The sparse kernels take the query blocks of each head in an order computed on the GPU
