@@ -8,6 +8,8 @@ from statistics import NormalDist
 import numpy as np
 import pytest
 import torch
+from hypothesis import given, settings
+from hypothesis import strategies as st
 
 from oracle import sol_attn_oracle as ora
 
@@ -281,6 +283,46 @@ def test_sparse_equals_dense_over_block_mean_keys(beta):
         want_nc = _brute_force_rows(qh[rows], kh, vh, scale, keymask)
         assert np.max(np.abs(sp["out"][0, 0, rows] - want_sp)) < 1e-12
         assert np.max(np.abs(nc["out"][0, 0, rows] - want_nc)) < 1e-12
+
+
+@settings(max_examples=40, deadline=None, derandomize=True)
+@given(n=st.integers(1, 60), bq=st.sampled_from([4, 8, 16, 32]), bk=st.sampled_from([4, 8, 16]),
+       d=st.integers(1, 4), forced=st.integers(0, 2), seed=st.integers(0, 10**6),
+       beta=st.one_of(st.floats(-2.0, 2.0), st.just(math.inf), st.just(-math.inf)))
+def test_closed_form_over_random_shapes(n, bq, bk, d, forced, seed, beta):
+    # The closed form of both sparse modes (see test_sparse_equals_dense_over_block_mean_keys)
+    # over random lengths, block sizes and forced tails: forced key blocks are always exact,
+    # an unselected routable block enters the corrected output through its mean key with
+    # its values unchanged, and the uncorrected output sees the kept keys only (a row with
+    # none is zero).
+    nk = -(-n // bk)
+    keep = forced * bk
+    if keep >= n or nk - forced < 1 or keep % bk or (n - keep) <= 0:
+        keep = 0
+    rng = np.random.default_rng(seed)
+    q, k, v = smooth_qkv(rng, B=1, H=1, N=n, d=d)
+    scale = 1 / math.sqrt(d)
+    sp = ora.forward(q, k, v, bq, bk, beta, "sparse", keep_tail_tokens=keep)
+    nc = ora.forward(q, k, v, bq, bk, beta, "sparse_no_correction", keep_tail_tokens=keep)
+    mask = sp["mask"][0, 0]
+    nkr = mask.shape[1]
+    assert nkr == nk - keep // bk
+    kh, vh, qh = k[0, 0], v[0, 0], q[0, 0]
+    for i in range(mask.shape[0]):
+        rows = slice(i * bq, min((i + 1) * bq, n))
+        kmod = kh.copy()
+        keymask = np.zeros(n, dtype=bool)
+        keymask[nkr * bk:] = True                    # forced tail
+        for j in range(nkr):
+            ks = slice(j * bk, min((j + 1) * bk, n))
+            if mask[i, j]:
+                keymask[ks] = True
+            else:
+                kmod[ks] = kh[ks].mean(axis=0)
+        want_sp = _brute_force_rows(qh[rows], kmod, vh, scale)
+        want_nc = _brute_force_rows(qh[rows], kh, vh, scale, keymask)
+        assert np.max(np.abs(sp["out"][0, 0, rows] - want_sp)) < 1e-11
+        assert np.max(np.abs(nc["out"][0, 0, rows] - want_nc)) < 1e-11
 
 
 def test_correction_is_exact_for_blockwise_constant_keys():
