@@ -924,17 +924,25 @@ __device__ __forceinline__ void lds_copy16(const void* base, uint32_t off, lds_p
     asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(m0) : "memory");
 }
 
-// Waves per SIMD the attention kernel is register-budgeted for: two, except where the LDS of a
-// workgroup (two 32 KB tile stages for d = 128) leaves room for only four waves per CU, i.e.
-// two-wave workgroups at d = 128, which then get the full register file.
+// Key split: at d = 128 the LDS of a workgroup (two 32 KB tile stages) leaves room for two
+// workgroups per CU, so a 64-row query block with one wave per 32 rows would run one wave per
+// SIMD.  Instead its workgroup has four waves: wave w owns rows 32*(w%2).. and the key half
+// w/2 (32 keys) of every tile, runs its own online softmax over those keys, and the two states
+// of each row merge at the end.  That gives two waves per SIMD with half the MFMAs per wave.
 template <int D, int BQ>
-constexpr int kAttnWavesPerEU = (D == 128 && BQ == 64) ? 1 : 2;
+constexpr bool kAttnKeySplit = (D == 128 && BQ == 64);
+template <int D, int BQ>
+constexpr int kAttnThreads = kAttnKeySplit<D, BQ> ? 256 : BQ * 2;
 
+// Every instantiation is register-budgeted for two waves per SIMD.
 template <int D, int BQ, int MODE, bool CAUSAL>
-__global__ __launch_bounds__(BQ * 2) __attribute__((amdgpu_waves_per_eu(kAttnWavesPerEU<D, BQ>, kAttnWavesPerEU<D, BQ>)))
+__global__ __launch_bounds__((kAttnThreads<D, BQ>)) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void routed_attn_kernel(AttnArgs a) {
-    constexpr int NT = BQ * 2;            // 64 threads per 32 query rows
+    constexpr bool KSPLIT = kAttnKeySplit<D, BQ>;
+    constexpr int NT = kAttnThreads<D, BQ>;   // 64 threads per 32 query rows (per key half)
     constexpr int NW = NT / 64;
+    constexpr int NS = KSPLIT ? 1 : 2;       // 32-key score M-tiles per wave and tile
+    constexpr int NPB = 2 * NS;              // 16-key P blocks per wave and tile
     using L = TileLds<D>;
     constexpr int KPW = L::KBYTES / 1024 / NW;   // direct-to-LDS wave loads per wave (K tile)
     constexpr int VPW = L::VBYTES / 1024 / NW;   // same for the V^T tile
@@ -963,6 +971,9 @@ void routed_attn_kernel(AttnArgs a) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, kept in an SGPR
     const int r32 = lane & 31, hh = lane >> 5;
+    const int rw = KSPLIT ? (wave & 1) : wave;   // 32-row slice of the query block
+    const int kh = KSPLIT ? (wave >> 1) : 0;     // key half of every tile (key split only)
+    const int kbase = 32 * kh;                   // first tile key of this wave's scores
 
     char* rest = smem + 2 * L::STAGE;
     int* scan_scratch = reinterpret_cast<int*>(rest);
@@ -991,7 +1002,7 @@ void routed_attn_kernel(AttnArgs a) {
     // slot of the ragged last key block among the correction slots (it can only be the last one)
     const int last_slot = (nuns > 0 && a.NKr == a.NK && ulist[max(nuns - 1, 0)] == a.NK - 1) ? nuns - 1 : -1;
 
-    const int qrow = qi * BQ + wave * 32 + r32;
+    const int qrow = qi * BQ + rw * 32 + r32;
     const uint16_t* qrow_p = a.q + ((size_t)bh * a.N + min(qrow, a.N - 1)) * D + 8 * hh;
     const int qlim = CAUSAL ? causal_lim(qrow, a.causal_g, a.N) : a.N;   // this lane's query sees keys < qlim
 
@@ -1117,13 +1128,15 @@ void routed_attn_kernel(AttnArgs a) {
     // LDS operand addresses: per lane, the chunk read at k-step ks of a K tile and at k-step
     // kk of a V^T tile (rows r32 and 32+r32 of K share the swizzle; the second M-tile is a
     // constant 8 KB further, V^T M-tiles 4 KB apart).  With the stage fixed at compile time
-    // every operand read is base register + immediate offset.
-    uint32_t kadr[NKS], vadr[4];
-#pragma unroll
-    for (int ks = 0; ks < NKS; ++ks) kadr[ks] = 16u * (uint32_t)L::kpos(r32, 2 * ks + hh);
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) vadr[kk] = (uint32_t)L::KBYTES + 16u * (uint32_t)L::vpos(r32, 2 * kk + hh);
+    // every operand read is base register + immediate offset.  Under the key split a wave reads
+    // K rows kbase.. and the V^T k-steps of its key half.
     constexpr int KT1 = 32 * L::KCPR * 16;   // byte offset of K rows 32..63
+    uint32_t kadr[NKS], vadr[NPB];
+#pragma unroll
+    for (int ks = 0; ks < NKS; ++ks) kadr[ks] = 16u * (uint32_t)L::kpos(r32, 2 * ks + hh) + (uint32_t)(kh * KT1);
+#pragma unroll
+    for (int kk = 0; kk < NPB; ++kk)
+        vadr[kk] = (uint32_t)L::KBYTES + 16u * (uint32_t)L::vpos(r32, 2 * (kk + NPB * kh) + hh);
     constexpr int VMT = 32 * L::VCPR * 16;   // byte offset between V^T M-tiles
     // Correction PV: the A operand (value means transposed: 32 values of d x 8 slots) of
     // M-tile mt and k-step kk comes from two transposed reads, slots 16kk + 4hh + 0..3 and
@@ -1136,7 +1149,7 @@ void routed_attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int mt = 0; mt < NDT; ++mt) {
             const int cc = 4 * mt + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
-            vtr[mt] = (uint32_t)(L::KBYTES + s0 * 2 * D + 16 * (cc ^ L::rswz(s0)) + 8 * (lane & 1));
+            vtr[mt] = (uint32_t)(L::KBYTES + (s0 + kbase) * 2 * D + 16 * (cc ^ L::rswz(s0)) + 8 * (lane & 1));
         }
     }
     auto ldv_apx = [&](int kk, int mt, int soff) SOL_INLINE -> f16x8 {
@@ -1156,42 +1169,42 @@ void routed_attn_kernel(AttnArgs a) {
         using AT = std::conditional_t<APX, f16x8, bf16x8>;
         AT a0[2], a1[2];
         a0[0] = *reinterpret_cast<const AT*>(smem + kadr[0] + SOFF);
-        a1[0] = *reinterpret_cast<const AT*>(smem + kadr[0] + SOFF + KT1);
+        if constexpr (NS == 2) a1[0] = *reinterpret_cast<const AT*>(smem + kadr[0] + SOFF + KT1);
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks) {
             if (ks + 1 < NKS) {
                 a0[(ks + 1) & 1] = *reinterpret_cast<const AT*>(smem + kadr[ks + 1] + SOFF);
-                a1[(ks + 1) & 1] = *reinterpret_cast<const AT*>(smem + kadr[ks + 1] + SOFF + KT1);
+                if constexpr (NS == 2) a1[(ks + 1) & 1] = *reinterpret_cast<const AT*>(smem + kadr[ks + 1] + SOFF + KT1);
             }
             if constexpr (APX) {
                 s0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a0[ks & 1], qop[ks], s0, 0, 0, 0);
-                s1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a1[ks & 1], qop[ks], s1, 0, 0, 0);
+                if constexpr (NS == 2) s1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(a1[ks & 1], qop[ks], s1, 0, 0, 0);
             } else {
                 s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[ks & 1], qop[ks], s0, 0, 0, 0);
-                s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks & 1], qop[ks], s1, 0, 0, 0);
+                if constexpr (NS == 2) s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[ks & 1], qop[ks], s1, 0, 0, 0);
             }
         }
     };
     // Keys past the end of the sequence (only in the last key block) -> -inf.
     auto mask_tail = [&](int j, f32x16& s0, f32x16& s1) SOL_INLINE {
-        const int nvalid = a.N - j * kBlockK;
-        if (nvalid < kBlockK) {
+        const int nvalid = a.N - j * kBlockK - kbase;
+        if (nvalid < kBlockK - kbase) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int key0 = 8 * (r >> 2) + 4 * hh + (r & 3);
                 if (key0 >= nvalid) s0[r] = kNegInf;
-                if (32 + key0 >= nvalid) s1[r] = kNegInf;
+                if (NS == 2 && 32 + key0 >= nvalid) s1[r] = kNegInf;
             }
         }
     };
     // Causal mask of a partially visible key block j: keys at or past this lane's limit -> -inf.
     auto mask_causal = [&](int j, f32x16& s0, f32x16& s1) SOL_INLINE {
-        const int rel = qlim - j * kBlockK;
+        const int rel = qlim - j * kBlockK - kbase;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int key0 = 8 * (r >> 2) + 4 * hh + (r & 3);
             if (key0 >= rel) s0[r] = kNegInf;
-            if (32 + key0 >= rel) s1[r] = kNegInf;
+            if (NS == 2 && 32 + key0 >= rel) s1[r] = kNegInf;
         }
     };
     // Correction tile of chunk c: slot j contributes with log2(n_j) (the multiplicity of Eq.
@@ -1200,8 +1213,8 @@ void routed_attn_kernel(AttnArgs a) {
         // Element r of this lane's score registers holds slot 4*hh + off(r) (s0) or 32 + that
         // (s1), off(r) = 8*(r/4) + r%4.  Slots below nv are unselected routable blocks and take
         // the multiplicity bias (log2 n_j); the rest of the last tile is padding.
-        int nv = nuns - c * kChunk - 4 * hh;      // off() bound of the valid slots
-        int last = last_slot - c * kChunk - 4 * hh;
+        int nv = nuns - c * kChunk - 4 * hh - kbase;      // off() bound of the valid slots
+        int last = last_slot - c * kChunk - 4 * hh - kbase;
         // opaque here, so that the 32 biases are formed where they are added and not hoisted
         // into the MFMA slots of the iteration, where they would hold 32 registers
         asm volatile("" : "+v"(nv), "+v"(last));
@@ -1211,7 +1224,7 @@ void routed_attn_kernel(AttnArgs a) {
             const float b0 = (off == last) ? a.bias_last : a.bias_full;
             const float b1 = (off + 32 == last) ? a.bias_last : a.bias_full;
             s0[r] += off < nv ? b0 : kNegInf;
-            s1[r] += off + 32 < nv ? b1 : kNegInf;
+            if constexpr (NS == 2) s1[r] += off + 32 < nv ? b1 : kNegInf;
         }
     };
     // Online softmax in the log2 domain with lazy rescaling, split so that the (rarely
@@ -1223,21 +1236,30 @@ void routed_attn_kernel(AttnArgs a) {
     //               P.  bo is a per-tile exponent offset: log2(64) for correction tiles whose
     //               64 slots are all full routable blocks (their multiplicity), else 0.
     auto tile_max = [&](const f32x16& s0, const f32x16& s1) SOL_INLINE -> float {
-        // balanced tree of three-input maxima over the lane's 32 scores (v_max3: 17 instructions,
-        // short dependency chains) ...
-        float x[32];
+        // balanced tree of three-input maxima over the lane's 32 (16 under the key split)
+        // scores (v_max3: 17 instructions for 32, short dependency chains) ...
+        float m0;
+        if constexpr (NS == 2) {
+            float x[32];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            x[r] = s0[r];
-            x[16 + r] = s1[r];
+            for (int r = 0; r < 16; ++r) {
+                x[r] = s0[r];
+                x[16 + r] = s1[r];
+            }
+            float a3[11];
+#pragma unroll
+            for (int i = 0; i < 10; ++i) a3[i] = fmaxf(fmaxf(x[3 * i], x[3 * i + 1]), x[3 * i + 2]);
+            a3[10] = fmaxf(x[30], x[31]);
+            const float b0 = fmaxf(fmaxf(a3[0], a3[1]), a3[2]), b1 = fmaxf(fmaxf(a3[3], a3[4]), a3[5]);
+            const float b2 = fmaxf(fmaxf(a3[6], a3[7]), a3[8]), b3 = fmaxf(a3[9], a3[10]);
+            m0 = fmaxf(fmaxf(fmaxf(b0, b1), b2), b3);
+        } else {
+            float a3[5];
+#pragma unroll
+            for (int i = 0; i < 5; ++i) a3[i] = fmaxf(fmaxf(s0[3 * i], s0[3 * i + 1]), s0[3 * i + 2]);
+            const float b0 = fmaxf(fmaxf(a3[0], a3[1]), a3[2]), b1 = fmaxf(fmaxf(a3[3], a3[4]), s0[15]);
+            m0 = fmaxf(b0, b1);
         }
-        float a3[11];
-#pragma unroll
-        for (int i = 0; i < 10; ++i) a3[i] = fmaxf(fmaxf(x[3 * i], x[3 * i + 1]), x[3 * i + 2]);
-        a3[10] = fmaxf(x[30], x[31]);
-        const float b0 = fmaxf(fmaxf(a3[0], a3[1]), a3[2]), b1 = fmaxf(fmaxf(a3[3], a3[4]), a3[5]);
-        const float b2 = fmaxf(fmaxf(a3[6], a3[7]), a3[8]), b3 = fmaxf(a3[9], a3[10]);
-        const float m0 = fmaxf(fmaxf(fmaxf(b0, b1), b2), b3);
         // ... then across the lane pair (l, l+32) that holds the query's other 32 keys, with a
         // VALU lane swap instead of an LDS permute
         const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(m0), __float_as_uint(m0), false, false);
@@ -1255,11 +1277,11 @@ void routed_attn_kernel(AttnArgs a) {
             m_run = mnew;
         }
     };
-    auto exps = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[4], float bo) SOL_INLINE {
+    auto exps = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[NPB], float bo) SOL_INLINE {
         const float msub = (m_run == kNegInf ? 0.f : m_run) - bo;
         const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
 #pragma unroll
-        for (int tt = 0; tt < 2; ++tt) {
+        for (int tt = 0; tt < NS; ++tt) {
 #pragma unroll
             for (int sh = 0; sh < 2; ++sh) {
 #pragma unroll
@@ -1277,12 +1299,12 @@ void routed_attn_kernel(AttnArgs a) {
             }
         }
     };
-    auto softmax = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[4], float bo) SOL_INLINE {
+    auto softmax = [&](const f32x16& s0, const f32x16& s1, f16x8 (&pb)[NPB], float bo) SOL_INLINE {
         rescale(tile_max(s0, s1) * cl + bo);
         exps(s0, s1, pb, bo);
     };
     // O^T += V^T P^T, operands double-buffered in registers.
-    auto pv = [&](auto apx_tag, auto stage_tag, const f16x8 (&pb)[4]) SOL_INLINE {
+    auto pv = [&](auto apx_tag, auto stage_tag, const f16x8 (&pb)[NPB]) SOL_INLINE {
         constexpr bool APX = decltype(apx_tag)::value;
         constexpr int SOFF = decltype(stage_tag)::value * L::STAGE;
         auto ld = [&](int kk, int mt) SOL_INLINE -> f16x8 {
@@ -1293,9 +1315,9 @@ void routed_attn_kernel(AttnArgs a) {
         av[0] = ld(0, 0);
         // kk-major: consecutive MFMAs update different accumulators (no dependent issue)
 #pragma unroll
-        for (int i = 0; i < NDT * 4; ++i) {
+        for (int i = 0; i < NDT * NPB; ++i) {
             const int kk = i / NDT, mt = i % NDT;
-            if (i + 1 < NDT * 4) av[(i + 1) & 1] = ld((i + 1) / NDT, (i + 1) % NDT);
+            if (i + 1 < NDT * NPB) av[(i + 1) & 1] = ld((i + 1) / NDT, (i + 1) % NDT);
             o[mt] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i & 1], pb[kk], o[mt], 0, 0, 0);
         }
     };
@@ -1375,7 +1397,8 @@ void routed_attn_kernel(AttnArgs a) {
         // 4k..4k+3); slots 16-31 run PV of tile t, which leaves their 16 MFMAs to hide the row
         // max of tile t+1 (finishing QK^T(t+1) early measured 1-2% faster than interleaving it
         // with PV(t)).  Successive MFMAs on one accumulator are at least two slots apart, and
-        // operands are read from LDS two slots ahead.
+        // operands are read from LDS two slots ahead.  Under the key split the same schedule has
+        // 8 + 8 slots (one 32-key score tile, two P blocks).
         // Generic iteration (any D): the same work in source order.
         auto step_generic = [&](auto par_tag, int t) SOL_INLINE {
             constexpr int P = decltype(par_tag)::value;
@@ -1385,7 +1408,7 @@ void routed_attn_kernel(AttnArgs a) {
             const int cn = t + 3 < T ? code(t + 3) : 0;
             f32x16 n0 = f32x16{}, n1 = f32x16{};
             qk(apx_tag, std::integral_constant<int, P ^ 1>{}, qop, n0, n1);
-            f16x8 pb[4];
+            f16x8 pb[NPB];
             exps(s0, s1, pb, bo);
             pv(apx_tag, par_tag, pb);
             bo = scores_done(t + 1, cv, n0, n1);
@@ -1407,7 +1430,7 @@ void routed_attn_kernel(AttnArgs a) {
             const int cn = t + 3 < T ? code(t + 3) : 0;
             const float msub = (m_run == kNegInf ? 0.f : m_run) - bo;
             const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
-            f16x8 pb[4];
+            f16x8 pb[NPB];
             auto exp_pair = [&](int kk, int q) SOL_INLINE {   // elements 2q, 2q+1 of P block kk
                 const int tt = kk >> 1, r = 8 * (kk & 1) + 2 * q;
                 const float x0 = tt ? s1[r] : s0[r];
@@ -1419,12 +1442,15 @@ void routed_attn_kernel(AttnArgs a) {
                 pb[kk][2 * q] = pp[0];
                 pb[kk][2 * q + 1] = pp[1];
             };
-            // slot -> operation: slots 0-15 QK^T (index i: k-step i/2, key half i%2), slots 16-31
-            // PV (index i: k-step i/4, d M-tile i%4)
-            auto kind = [](int sl) SOL_INLINE { return sl < 16 ? 0 : 1; };
-            auto index = [](int sl) SOL_INLINE { return sl < 16 ? sl : sl - 16; };
+            // slot -> operation: slots 0..NQK-1 QK^T (index i: k-step i/NS, key half i%NS), the
+            // rest PV (index i: k-step i/4, d M-tile i%4).  Under the key split a wave has 8 + 8
+            // slots, each of the first 8 with one exponential pair.
+            constexpr int NQK = NKS * NS, NSLOT = NQK + NPB * NDT;
+            auto kind = [](int sl) SOL_INLINE { return sl < NQK ? 0 : 1; };
+            auto index = [](int sl) SOL_INLINE { return sl < NQK ? sl : sl - NQK; };
             auto ldk = [&](int qi) SOL_INLINE {
-                return *reinterpret_cast<const KT*>(smem + kadr[qi >> 1] + KOFF + (qi & 1) * KT1);
+                if constexpr (NS == 1) return *reinterpret_cast<const KT*>(smem + kadr[qi] + KOFF);
+                else return *reinterpret_cast<const KT*>(smem + kadr[qi >> 1] + KOFF + (qi & 1) * KT1);
             };
             auto ldv = [&](int pi) SOL_INLINE -> f16x8 {
                 if constexpr (APX) return ldv_apx(pi >> 2, pi & 3, VOFF);
@@ -1434,7 +1460,7 @@ void routed_attn_kernel(AttnArgs a) {
             f16x8 vop[4];
             int nk = 0, nv = 0;   // operands loaded so far (ring of 4)
             auto prefetch = [&](int sl) SOL_INLINE {
-                if (sl >= 32) return;
+                if (sl >= NSLOT) return;
                 if (kind(sl) == 0) kop[(nk++) & 3] = ldk(index(sl));
                 else vop[(nv++) & 3] = ldv(index(sl));
             };
@@ -1443,18 +1469,19 @@ void routed_attn_kernel(AttnArgs a) {
             prefetch(1);
             int uk = 0, uv = 0;   // operands consumed so far
 #pragma unroll
-            for (int sl = 0; sl < 32; ++sl) {
+            for (int sl = 0; sl < NSLOT; ++sl) {
                 prefetch(sl + 2);
                 const int id = index(sl);
                 if (kind(sl) == 0) {
                     const KT av = kop[(uk++) & 3];
-                    if (id & 1) n1 = mfma_qk(av, qop[id >> 1], n1);
+                    if (NS == 1) n0 = mfma_qk(av, qop[id], n0);
+                    else if (id & 1) n1 = mfma_qk(av, qop[id >> 1], n1);
                     else n0 = mfma_qk(av, qop[id >> 1], n0);
                 } else {
                     const f16x8 av = vop[(uv++) & 3];
                     o[id & 3] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, pb[id >> 2], o[id & 3], 0, 0, 0);
                 }
-                if (sl < 16) exp_pair(sl >> 2, sl & 3);
+                if (sl < 4 * NPB) exp_pair(sl >> 2, sl & 3);
             }
             bo = scores_done(t + 1, cv, n0, n1);
             mx = tile_max_l2(n0, n1, bo);
@@ -1481,7 +1508,7 @@ void routed_attn_kernel(AttnArgs a) {
         // last tile (t == T-1): its max is taken again here, after the bias or the tail mask
         if constexpr (APX) bias_apx(code(T - 1), s0, s1);
         else mask_tail(code(T - 1), s0, s1);
-        f16x8 pb[4];
+        f16x8 pb[NPB];
         softmax(s0, s1, pb, bo);
         if ((T - 1) & 1) pv(apx_tag, S1{}, pb);
         else pv(apx_tag, S0{}, pb);
@@ -1510,19 +1537,74 @@ void routed_attn_kernel(AttnArgs a) {
     // ---- epilogue: O = O^T / l, bf16
     const float lsum = (l_run[0] + l_run[1]) + (l_run[2] + l_run[3]);
     const float lt = lsum + __shfl_xor(lsum, 32);
-    const float inv = lt > 0.f ? 1.0f / lt : 0.f;
-    if (qrow < a.N) {
-        uint16_t* op = a.out + ((size_t)bh * a.N + qrow) * D;
+    uint16_t* op = a.out + ((size_t)bh * a.N + qrow) * D;   // written only for rows < N
+    auto store = [&](int mt, const f32x16& v, float inv) SOL_INLINE {   // d rows 32mt.. of O^T
 #pragma unroll
-        for (int mt = 0; mt < NDT; ++mt) {
+        for (int i = 0; i < 4; ++i) {
+            const int d0 = 32 * mt + 8 * i + 4 * hh;
+            uint32_t w0 = (uint32_t)f32_to_bf16_bits(v[4 * i + 0] * inv) |
+                          ((uint32_t)f32_to_bf16_bits(v[4 * i + 1] * inv) << 16);
+            uint32_t w1 = (uint32_t)f32_to_bf16_bits(v[4 * i + 2] * inv) |
+                          ((uint32_t)f32_to_bf16_bits(v[4 * i + 3] * inv) << 16);
+            *reinterpret_cast<uint2*>(op + d0) = make_uint2(w0, w1);
+        }
+    };
+    if constexpr (!KSPLIT) {
+        const float inv = lt > 0.f ? 1.0f / lt : 0.f;
+        if (qrow < a.N) {
+#pragma unroll
+            for (int mt = 0; mt < NDT; ++mt) store(mt, o[mt], inv);
+        }
+    } else {
+        // The two key halves of a row hold separate softmax states (m, l, O) over disjoint keys.
+        // Wave (rw, kh) finishes d M-tiles 2kh and 2kh+1: it hands its other two M-tiles, its
+        // running max and its row sum to its partner (rw, 1-kh) through LDS (the tile stages are
+        // free once every wave is past its last PV), takes the partner's copy of its own two, and
+        // rescales both states to the common max: O = (a0 O0 + a1 O1) / (a0 l0 + a1 l1).
+        static_assert(NDT == 4, "the key split assumes d = 128");
+        constexpr int XREG = 2 * 16 * 64 + 2 * 64;   // floats per wave: 2 M-tiles, m, l
+        static_assert(4 * XREG * 4 <= 2 * L::STAGE, "exchange buffer exceeds the tile stages");
+        float* xbuf = reinterpret_cast<float*>(smem);
+        __syncthreads();
+        float* mine = xbuf + wave * XREG;
+        auto put = [&](const f32x16& v0, const f32x16& v1) SOL_INLINE {   // lane-contiguous 16 B
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int d0 = 32 * mt + 8 * i + 4 * hh;
-                uint32_t w0 = (uint32_t)f32_to_bf16_bits(o[mt][4 * i + 0] * inv) |
-                              ((uint32_t)f32_to_bf16_bits(o[mt][4 * i + 1] * inv) << 16);
-                uint32_t w1 = (uint32_t)f32_to_bf16_bits(o[mt][4 * i + 2] * inv) |
-                              ((uint32_t)f32_to_bf16_bits(o[mt][4 * i + 3] * inv) << 16);
-                *reinterpret_cast<uint2*>(op + d0) = make_uint2(w0, w1);
+                *reinterpret_cast<float4*>(mine + (i * 64 + lane) * 4) = make_float4(v0[4 * i], v0[4 * i + 1], v0[4 * i + 2], v0[4 * i + 3]);
+                *reinterpret_cast<float4*>(mine + ((4 + i) * 64 + lane) * 4) = make_float4(v1[4 * i], v1[4 * i + 1], v1[4 * i + 2], v1[4 * i + 3]);
+            }
+        };
+        if (kh == 0) put(o[2], o[3]);
+        else put(o[0], o[1]);
+        mine[2048 + lane] = m_run;
+        mine[2048 + 64 + lane] = lt;
+        __syncthreads();
+        const float* theirs = xbuf + (wave ^ 2) * XREG;
+        const float mp = theirs[2048 + lane], lp = theirs[2048 + 64 + lane];
+        const float mm = fmaxf(m_run, mp);
+        const float a0 = m_run == kNegInf ? 0.f : __builtin_amdgcn_exp2f(m_run - mm);
+        const float a1 = mp == kNegInf ? 0.f : __builtin_amdgcn_exp2f(mp - mm);
+        const float l = a0 * lt + a1 * lp;
+        const float inv = l > 0.f ? 1.0f / l : 0.f;
+        auto merged = [&](const f32x16& own, int half) SOL_INLINE -> f32x16 {
+            f32x16 r;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float4 p = *reinterpret_cast<const float4*>(theirs + ((4 * half + i) * 64 + lane) * 4);
+                r[4 * i + 0] = a0 * own[4 * i + 0] + a1 * p.x;
+                r[4 * i + 1] = a0 * own[4 * i + 1] + a1 * p.y;
+                r[4 * i + 2] = a0 * own[4 * i + 2] + a1 * p.z;
+                r[4 * i + 3] = a0 * own[4 * i + 3] + a1 * p.w;
+            }
+            return r;
+        };
+        if (qrow < a.N) {
+            if (kh == 0) {
+                store(0, merged(o[0], 0), inv);
+                store(1, merged(o[1], 1), inv);
+            } else {
+                store(2, merged(o[2], 0), inv);
+                store(3, merged(o[3], 1), inv);
             }
         }
     }
@@ -1680,7 +1762,7 @@ hipError_t launch_attn_bf16(const Shape& s, const AttnArgs& a, hipStream_t st) {
     hipError_t e = allow_lds(kern, lds);
     if (e != hipSuccess) return e;
     const int grid = 8 * a.per_x * a.BH;
-    kern<<<dim3(grid), dim3(BQ * 2), lds, st>>>(a);
+    kern<<<dim3(grid), dim3(kAttnThreads<D, BQ>), lds, st>>>(a);
     return hipGetLastError();
 }
 

@@ -114,6 +114,9 @@ EDGE = {
     "n65": ((5, 13), 128, 128, "bf16", 0, 2, 3),          # B=2, H=3; a 1-token last key block
     "one_routable": ((1, 64), 128, 64, "bf16", 64, 1, 2), # N=128 with 64 text tokens: one routable block
     "f32_n100": ((10, 10), 64, 128, "f32", 0, 2, 1),      # f32 path, ragged, B=2
+    "split_tail13": ((5, 41), 128, 64, "bf16", 0, 1, 2),  # d=128, 64-row blocks: last key block 13 keys,
+                                                          # its second 32-key half empty
+    "split_tail32": ((4, 40), 128, 64, "bf16", 0, 2, 1),  # last key block exactly one 32-key half
 }
 
 
@@ -258,8 +261,11 @@ def test_thresholds_parity_diagonal(dev, name, beta):
         np.testing.assert_allclose(to_np(tau), tau_r, atol=1e-5, rtol=1e-5)
 
 
-def test_beta_minus_inf_is_bitwise_dense(dev):
-    w, (q, k, v) = small_inputs("bf16_d128_q128")
+@pytest.mark.parametrize("name", ["bf16_d128_q128", "bf16_d128_q64_text", "bf16_d64_q64_text"])
+def test_beta_minus_inf_is_bitwise_dense(dev, name):
+    # every routable block selected: the exact tiles are all key blocks in increasing order, as in
+    # dense mode, so the two outputs agree bit for bit (any query-block height and key split)
+    w, (q, k, v) = small_inputs(name)
     dense, _, _ = run_gpu(dev, w, q, k, v, 0.0, "dense", want_mask=False)
     for mode in ("sparse", "sparse_no_correction"):
         out, gmask, counts = run_gpu(dev, w, q, k, v, -INF, mode)
@@ -300,8 +306,9 @@ def test_caller_workspace(dev):
     assert ei.value.code == sb.SOL_ERR_WORKSPACE
 
 
-def test_deterministic(dev):
-    w, (q, k, v) = small_inputs("bf16_d128_q128")
+@pytest.mark.parametrize("name", ["bf16_d128_q128", "bf16_d128_q64_text"])
+def test_deterministic(dev, name):
+    w, (q, k, v) = small_inputs(name)
     a, _, _ = run_gpu(dev, w, q, k, v, 0.8, "sparse")
     b, _, _ = run_gpu(dev, w, q, k, v, 0.8, "sparse")
     assert torch.equal(a, b)
