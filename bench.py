@@ -34,9 +34,9 @@ KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_24027_amd", "csrc", "sol_attn_ker
 # then WRITE_SIZE), each scaled by what the same counter reads for the 1 GiB calibration copy
 # (FETCH x 2.000, WRITE x 1.000).  Valid only for the kernel source and workload it was taken on.
 MEASURED_TRAFFIC = {
-    "kernel_sha256": "4c59abda32c7d80fceb5c615212bc03c35ddff42457324bb5a43075693b81daf",
+    "kernel_sha256": "595e61fee6116d545e7b250e9383737b77371a75f3904e9fa2e49e1d213f4a45",
     "workload": "video720p", "kept": 0.2,
-    "fetch_bytes": 103.60e9, "write_bytes": 0.7759e9,
+    "fetch_bytes": 68.98e9, "write_bytes": 0.7759e9,
 }
 
 

@@ -1013,7 +1013,41 @@ void routed_attn_kernel(AttnArgs a) {
     // that the dot-product accumulations of a tile form four short dependency chains.
     float m_run = kNegInf, l_run[4] = {0.f, 0.f, 0.f, 0.f};
 
-    auto tile_code = [&](int n) -> int { return MODE == kDense ? n : (int)elist[n]; };
+    // Start phase of the exact tiles (sparse modes, no causal mask).  A workgroup walks its
+    // selected blocks in increasing order.  The 64 workgroups resident on an XCD (two per CU)
+    // start together at block 0; later ones start whenever a slot frees, while the others are
+    // part-way through their lists, so their tiles are no longer in L2 when the newcomer asks
+    // for them.  The y-th workgroup of an XCD's stream (y >= 64) therefore starts its walk at
+    // block j0 = ((y - 64) mod 64) / 64 of the unselected count and wraps round, which spreads
+    // the newcomers over the key range the way the running ones are spread.  With every block
+    // selected j0 = 0, so that case keeps dense mode's tile order exactly.  The ragged last key
+    // block, when selected, stays the last tile (its tail mask is applied after the loop).
+    int k0 = 0, nrot = 0;
+    if constexpr (MODE != kDense && !CAUSAL) {
+        const bool ragged_last = nsel > 0 && a.NKr == a.NK && (a.N % kBlockK) != 0 && elist[nsel - 1] == a.NK - 1;
+        nrot = nsel - (ragged_last ? 1 : 0);
+        constexpr int kResident = 64;   // workgroups resident per XCD: 2 per CU x 32 CUs
+        const int j0 = y < kResident ? 0 : ((y - kResident) % kResident) * (a.NKr - nsel) / kResident;
+        int lo = 0, hi = nrot;          // first position with elist[k] >= j0
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if ((int)elist[mid] < j0) lo = mid + 1;
+            else hi = mid;
+        }
+        k0 = lo < nrot ? lo : 0;
+        k0 = __builtin_amdgcn_readfirstlane(k0);
+    }
+    auto tile_code = [&](int n) -> int {
+        if constexpr (MODE == kDense) return n;
+        else {
+            int k = n;
+            if (n < nrot) {
+                k = n + k0;
+                if (k >= nrot) k -= nrot;
+            }
+            return (int)elist[k];
+        }
+    };
     // Global->LDS copies.  Each lane moves one 16-byte chunk per instruction; the per-lane
     // byte offsets inside a tile are fixed, so they are computed once here and each tile only
     // adds wave-uniform base pointers.  Rows past the end of the sequence (ragged last block)
