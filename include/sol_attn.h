@@ -147,7 +147,10 @@ int sol_attn_forward(const void* q, const void* k, const void* v, void* out,
  *   in the routing statistics or the counts.  0 for none.
  * workspace/workspace_bytes: caller device scratch of at least
  *   sol_attn_workspace_bytes(...) bytes, or NULL/0 to let the library allocate
- *   (and keep, growing on demand) its own.
+ *   (and keep, growing on demand) its own.  It holds the pre-pass results and
+ *   the fused kernel's work-queue counters, so two calls that may run at the
+ *   same time (different streams) need different workspaces; calls that pass
+ *   NULL share the library's one per device.
  * counts: [B,H] u32 device, or NULL for a library buffer.  After the call,
  *   counts[b*H+h] = number of (query block, routable key block) pairs selected
  *   for exact computation (all routable pairs in SOL_DENSE).
@@ -161,8 +164,13 @@ int sol_attn_forward(const void* q, const void* k, const void* v, void* out,
  * Selection is computed on chip from f32 pooled proxies s*Qbar_i.Kbar_j and
  * never written to memory unless mask_out is given.  In the sparse modes the
  * library also orders the query blocks of each head by their pooled queries, so
- * that blocks with similar selections run together and share L2; this changes
- * only which workgroup computes which block, never a result.
+ * that blocks with similar selections run together and share L2, and starts a
+ * block's walk over its selected key blocks at a phase set by its place in that
+ * schedule.  Neither changes which blocks are selected; the start phase changes
+ * the order in which a block's exact tiles are accumulated, so results differ
+ * from an increasing-order walk by rounding only.  Both are functions of the
+ * inputs, so results are deterministic, and with every block selected the walk
+ * starts at block 0, so tau = -INFINITY reproduces SOL_DENSE bit for bit.
  */
 int sol_attn_forward_ex(const void* q, const void* k, const void* v, void* out,
                         int B, int H, int N, int d, int block_q, int block_k,

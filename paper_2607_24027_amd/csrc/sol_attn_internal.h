@@ -46,6 +46,7 @@ struct Workspace {
     uint16_t* order = nullptr;   // [BH][NQ] query-block order of the sparse kernels
     double* mom = nullptr;       // partial moments, moments_scratch_bytes()
     uint32_t* blkcount = nullptr;// [BH][NQ]
+    uint32_t* queue = nullptr;   // [8][32] per-XCD claim counters of the bf16 attention kernel (one per 128 B)
 };
 
 // Returns the byte size; fills *ws when base != nullptr.

@@ -23,6 +23,7 @@
 // 8 keys a lane contributes contiguous in LDS.
 #include "sol_attn_internal.h"
 
+#include <algorithm>
 #include <cmath>
 #include <type_traits>
 
@@ -666,7 +667,9 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
     constexpr int CPT = CPR / TPK;          // 16-byte chunks of a row per thread
     constexpr int KPWV = 64 / TPK;          // pooled keys per wave (64, 32 or 16)
     static_assert(NT % kChunk == 0 && TPK <= 4, "routing expects 64..256 threads");
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int tid_ = threadIdx.x;
+    asm volatile("" : "+v"(tid_));   // per-lane values formed here, not hoisted out of a block loop
+    const int tid = tid_, lane = tid & 63, wave = tid >> 6;
     const int jl = tid / TPK, seg = tid % TPK;
     // Each thread streams its share (chunks seg, seg+TPK, ...) of one pooled-key row per group
     // of 64 keys straight from L2 into registers, up to three groups in flight; the pooled
@@ -826,6 +829,7 @@ struct AttnArgs {
     uint32_t* blkcount;
     uint32_t* mask_out;
     const uint16_t* order;        // [BH][NQ] query-block order (sparse modes), or null: identity
+    uint32_t* queue;              // [8][32] per-XCD claim counters, zero at launch
     int BH, N, NQ, NK, NKr, NC, MW, per_x;
     float scale, c_log2;
     float bias_full, bias_last;   // log2(n_j)/c_log2 for full blocks and for the last block
@@ -935,9 +939,9 @@ template <int D, int BQ>
 constexpr int kAttnThreads = kAttnKeySplit<D, BQ> ? 256 : BQ * 2;
 
 // Every instantiation is register-budgeted for two waves per SIMD.
+// One query block (b, h, qi) of the fused kernel; y is its position in its XCD's queue.
 template <int D, int BQ, int MODE, bool CAUSAL>
-__global__ __launch_bounds__((kAttnThreads<D, BQ>)) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void routed_attn_kernel(AttnArgs a) {
+__device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const int bh, const int qi, const int y) {
     constexpr bool KSPLIT = kAttnKeySplit<D, BQ>;
     constexpr int NT = kAttnThreads<D, BQ>;   // 64 threads per 32 query rows (per key half)
     constexpr int NW = NT / 64;
@@ -948,27 +952,13 @@ void routed_attn_kernel(AttnArgs a) {
     constexpr int VPW = L::VBYTES / 1024 / NW;   // same for the V^T tile
     constexpr int NDT = D / 32;           // output M-tiles (d rows)
     constexpr int NKS = D / 16;           // k-steps of QK^T
-    extern __shared__ __attribute__((aligned(16))) char smem[];
 
-    // XCD-aware mapping: consecutive workgroups go round-robin to the 8 XCDs, so XCD x gets
-    // a contiguous range of query blocks of the current head.  Under a causal mask the work
-    // of a query block grows with its index, so the head's blocks are cut into 16 segments
-    // and XCD x takes segment 15 - x (descending, the longer blocks first) and then segment
-    // x: every XCD gets the same amount of work.
-    const int wg = blockIdx.x;
-    const int xcd = wg & 7, y = wg >> 3;
-    const int bh = y / a.per_x;
-    int qi;
-    if constexpr (CAUSAL) {
-        const int u = y % a.per_x, hp = a.per_x >> 1;
-        qi = u < hp ? (15 - xcd) * hp + (hp - 1 - u) : xcd * hp + (u - hp);
-    } else {
-        qi = xcd * a.per_x + (y % a.per_x);
-        if (a.order != nullptr && bh < a.BH && qi < a.NQ) qi = a.order[(size_t)bh * a.NQ + qi];
-    }
-    if (bh >= a.BH || qi >= a.NQ) return;
-
-    const int tid = threadIdx.x, lane = tid & 63;
+    // The thread index is made opaque here so that the per-lane constants derived from it are
+    // formed anew for every block rather than hoisted out of the block loop, where they would
+    // stay live through it and push the tile loop past its register budget.
+    int tid_ = threadIdx.x;
+    asm volatile("" : "+v"(tid_));
+    const int tid = tid_, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, kept in an SGPR
     const int r32 = lane & 31, hh = lane >> 5;
     const int rw = KSPLIT ? (wave & 1) : wave;   // 32-row slice of the query block
@@ -1013,13 +1003,13 @@ void routed_attn_kernel(AttnArgs a) {
     // that the dot-product accumulations of a tile form four short dependency chains.
     float m_run = kNegInf, l_run[4] = {0.f, 0.f, 0.f, 0.f};
 
-    // Start phase of the exact tiles (sparse modes, no causal mask).  A workgroup walks its
-    // selected blocks in increasing order.  The 64 workgroups resident on an XCD (two per CU)
-    // start together at block 0; later ones start whenever a slot frees, while the others are
-    // part-way through their lists, so their tiles are no longer in L2 when the newcomer asks
-    // for them.  The y-th workgroup of an XCD's stream (y >= 64) therefore starts its walk at
-    // block j0 = ((y - 64) mod 64) / 64 of the unselected count and wraps round, which spreads
-    // the newcomers over the key range the way the running ones are spread.  With every block
+    // Start phase of the exact tiles (sparse modes, no causal mask).  A block walks its selected
+    // key blocks in increasing order.  The first 64 blocks of an XCD's queue (two workgroups per
+    // CU) start together at key block 0; later ones start whenever a workgroup finishes, while
+    // the others are part-way through their lists, so their tiles are no longer in L2 when the
+    // newcomer asks for them.  The block at queue position y >= 64 therefore starts its walk at
+    // j0 = ((y - 64) mod 64) / 64 of the unselected count and wraps round, which spreads the
+    // newcomers over the key range the way the running blocks are spread.  With every block
     // selected j0 = 0, so that case keeps dense mode's tile order exactly.  The ragged last key
     // block, when selected, stays the last tile (its tail mask is applied after the loop).
     int k0 = 0, nrot = 0;
@@ -1644,6 +1634,79 @@ void routed_attn_kernel(AttnArgs a) {
     }
 }
 
+// The fused kernel runs persistent workgroups (as many as fit on the device at once) that
+// claim query blocks from eight queues, one per XCD.  Queue x lists, in order, the blocks of
+// a fixed XCD-aware assignment: position y holds block y % per_x of XCD x's contiguous range
+// of head y / per_x (through the query-block order in the sparse modes), so the workgroups
+// resident on one XCD work through neighbouring blocks of one head and share its K/V in
+// their L2.  Under a causal mask the work of a query block grows with its index, so the
+// head's blocks are cut into 16 segments and queue x takes segment 15 - x (descending, the
+// longer blocks first) and then segment x.  Consecutive workgroups go round-robin to the 8
+// XCDs, so workgroup w serves queue w & 7 first; once that queue is empty it takes blocks
+// from the queue with the most left.  XCDs whose blocks need more tiles, or that run slower,
+// thus get help at the end instead of finishing last.  A block's result does not depend on
+// which workgroup computes it, and every claim either takes a block or finds a queue empty
+// for good, so each workgroup stops after at most eight failed claims.
+template <int D, int BQ, int MODE, bool CAUSAL>
+__global__ __launch_bounds__((kAttnThreads<D, BQ>)) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void routed_attn_kernel(AttnArgs a) {
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    __shared__ int s_task[2];
+    const int home = blockIdx.x & 7;
+    const unsigned qlen = (unsigned)a.per_x * (unsigned)a.BH;   // positions per queue
+    for (;;) {
+        __syncthreads();   // the previous block is done with LDS and with s_task
+        // Claims are made when a block starts, not ahead of it: a queue position then also
+        // orders the blocks by start time, which the exact tiles' start phase relies on.
+        if (threadIdx.x == 0) {
+            int tx = -1;
+            unsigned tp = 0;
+            const unsigned p = atomicAdd(a.queue + 32 * home, 1u);
+            if (p < qlen) {
+                tx = home;
+                tp = p;
+            } else {
+                for (int tries = 0; tries < 8 && tx < 0; ++tries) {
+                    int best = -1;
+                    unsigned left = 0;
+                    for (int x = 0; x < 8; ++x) {
+                        const unsigned c = __hip_atomic_load(a.queue + 32 * x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        if (c < qlen && qlen - c > left) {
+                            left = qlen - c;
+                            best = x;
+                        }
+                    }
+                    if (best < 0) break;
+                    const unsigned q = atomicAdd(a.queue + 32 * best, 1u);
+                    if (q < qlen) {
+                        tx = best;
+                        tp = q;
+                    }
+                }
+            }
+            s_task[0] = tx;
+            s_task[1] = (int)tp;
+        }
+        __syncthreads();
+        const int x = s_task[0], y = s_task[1];
+        if (x < 0) return;
+        const int bh = y / a.per_x;
+        int qi;
+        if constexpr (CAUSAL) {
+            const int u = y % a.per_x, hp = a.per_x >> 1;
+            qi = u < hp ? (15 - x) * hp + (hp - 1 - u) : x * hp + (u - hp);
+        } else {
+            qi = x * a.per_x + (y % a.per_x);
+            if (a.order != nullptr && qi < a.NQ) qi = a.order[(size_t)bh * a.NQ + qi];
+        }
+        if (qi < a.NQ) attn_block<D, BQ, MODE, CAUSAL>(a, smem, bh, qi, y);
+    }
+}
+
+__global__ void queue_reset_kernel(uint32_t* q) {
+    if (threadIdx.x < 8) q[32 * threadIdx.x] = 0u;
+}
+
 // ---------------------------------------------------------------------------
 // Routed attention with f32 inputs (correctness-first path, VALU only).  One thread per
 // query row; K/V (or pooled Kbar/Vbar for correction tiles) staged in LDS one tile at a
@@ -1795,8 +1858,16 @@ hipError_t launch_attn_bf16(const Shape& s, const AttnArgs& a, hipStream_t st) {
     auto kern = routed_attn_kernel<D, BQ, MODE, CAUSAL>;
     hipError_t e = allow_lds(kern, lds);
     if (e != hipSuccess) return e;
-    const int grid = 8 * a.per_x * a.BH;
-    kern<<<dim3(grid), dim3(kAttnThreads<D, BQ>), lds, st>>>(a);
+    // persistent grid: as many workgroups as fit at once, a multiple of 8 (one share per XCD),
+    // never more than there are query-block positions
+    int dev = 0, cus = 0, occ = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, kAttnThreads<D, BQ>, lds)) != hipSuccess) return e;
+    const long long positions = 8LL * a.per_x * a.BH;
+    long long grid = ((long long)std::max(cus * std::max(occ, 1), 8) / 8) * 8;
+    grid = std::min(grid, positions);
+    kern<<<dim3((unsigned)grid), dim3(kAttnThreads<D, BQ>), lds, st>>>(a);
     return hipGetLastError();
 }
 
@@ -1901,6 +1972,7 @@ size_t workspace_layout(const Shape& s, char* base, Workspace* ws) {
         w.vbar = reinterpret_cast<float*>(take(BH * s.NK * d * 4));
     }
     w.blkcount = reinterpret_cast<uint32_t*>(take(BH * s.NQ * 4));
+    if (s.dtype == kBF16) w.queue = reinterpret_cast<uint32_t*>(take(8 * 32 * 4));
     if (ws) *ws = w;
     return off;
 }
@@ -1981,6 +2053,7 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         }
         AttnArgs a{};
         a.order = (routing && !s.causal) ? ws.order : nullptr;
+        a.queue = ws.queue;
         a.q = static_cast<const uint16_t*>(q);
         a.k = kk;
         a.vt = ws.vt;
@@ -2000,6 +2073,8 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         a.c_log2 = scale * kLog2e;
         a.bias_full = log2f((float)kBlockK) / a.c_log2;
         a.bias_last = log2f((float)(s.N - (s.NK - 1) * kBlockK)) / a.c_log2;
+        queue_reset_kernel<<<1, 64, 0, st>>>(ws.queue);   // a fill kernel, not a memset: safe under graph capture
+        if ((e = hipGetLastError()) != hipSuccess) return e;
         if (ev_start && (e = hipEventRecord(ev_start, st)) != hipSuccess) return e;
         if (d == 128) e = s.bq == 128 ? dispatch_bf16<128, 128>(s, a, st) : dispatch_bf16<128, 64>(s, a, st);
         else e = s.bq == 128 ? dispatch_bf16<64, 128>(s, a, st) : dispatch_bf16<64, 64>(s, a, st);
