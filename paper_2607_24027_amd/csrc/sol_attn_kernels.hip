@@ -1415,6 +1415,9 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
         qk(apx_tag, S0{}, qop, s0, s1);
         float bo = scores_done(0, c0, s0, s1);   // offset of the tile whose scores are in s0/s1
         float mx = tile_max_l2(s0, s1, bo);
+        // The first step refills stage 0's K region (tile 2) that QK^T(0) has just read; every
+        // later refill of a region follows the barrier that ends the iteration which read it.
+        if (T > 2) __syncthreads();
         // iteration t with t & 1 == P: K of tile t+1 in stage P^1, V of tile t in stage P
         // D = 128: one pipelined iteration as 32 MFMA slots.  Slots 0-15 run QK^T of tile t+1
         // while the exponentials of tile t are formed (one pair per slot, P block k in slots
