@@ -830,6 +830,7 @@ struct AttnArgs {
     uint32_t* mask_out;
     const uint16_t* order;        // [BH][NQ] query-block order (sparse modes), or null: identity
     uint32_t* queue;              // [8][32] per-XCD claim counters, zero at launch
+    int resident;                 // workgroups per XCD in the persistent grid (grid / 8)
     int BH, N, NQ, NK, NKr, NC, MW, per_x;
     float scale, c_log2;
     float bias_full, bias_last;   // log2(n_j)/c_log2 for full blocks and for the last block
@@ -1004,20 +1005,21 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
     float m_run = kNegInf, l_run[4] = {0.f, 0.f, 0.f, 0.f};
 
     // Start phase of the exact tiles (sparse modes, no causal mask).  A block walks its selected
-    // key blocks in increasing order.  The first 64 blocks of an XCD's queue (two workgroups per
-    // CU) start together at key block 0; later ones start whenever a workgroup finishes, while
-    // the others are part-way through their lists, so their tiles are no longer in L2 when the
-    // newcomer asks for them.  The block at queue position y >= 64 therefore starts its walk at
-    // j0 = ((y - 64) mod 64) / 64 of the unselected count and wraps round, which spreads the
-    // newcomers over the key range the way the running blocks are spread.  With every block
-    // selected j0 = 0, so that case keeps dense mode's tile order exactly.  The ragged last key
-    // block, when selected, stays the last tile (its tail mask is applied after the loop).
+    // key blocks in increasing order.  The first R blocks of an XCD's queue (R = the workgroups
+    // of the persistent grid on one XCD, 64 at d = 128) start together at key block 0; later ones
+    // start whenever a workgroup finishes, while the others are part-way through their lists,
+    // so their tiles are no longer in L2 when the newcomer asks for them.  The block at queue
+    // position y >= R therefore starts its walk at j0 = ((y - R) mod R) / R of the unselected
+    // count and wraps round, which spreads the newcomers over the key range the way the running
+    // blocks are spread.  With every block selected j0 = 0, so that case keeps dense mode's tile
+    // order exactly.  The ragged last key block, when selected, stays the last tile (its tail
+    // mask is applied after the loop).
     int k0 = 0, nrot = 0;
     if constexpr (MODE != kDense && !CAUSAL) {
         const bool ragged_last = nsel > 0 && a.NKr == a.NK && (a.N % kBlockK) != 0 && elist[nsel - 1] == a.NK - 1;
         nrot = nsel - (ragged_last ? 1 : 0);
-        constexpr int kResident = 64;   // workgroups resident per XCD: 2 per CU x 32 CUs
-        const int j0 = y < kResident ? 0 : ((y - kResident) % kResident) * (a.NKr - nsel) / kResident;
+        const int R = a.resident;
+        const int j0 = y < R ? 0 : ((y - R) % R) * (a.NKr - nsel) / R;
         int lo = 0, hi = nrot;          // first position with elist[k] >= j0
         while (lo < hi) {
             const int mid = (lo + hi) >> 1;
@@ -1870,7 +1872,9 @@ hipError_t launch_attn_bf16(const Shape& s, const AttnArgs& a, hipStream_t st) {
     const long long positions = 8LL * a.per_x * a.BH;
     long long grid = ((long long)std::max(cus * std::max(occ, 1), 8) / 8) * 8;
     grid = std::min(grid, positions);
-    kern<<<dim3((unsigned)grid), dim3(kAttnThreads<D, BQ>), lds, st>>>(a);
+    AttnArgs b = a;
+    b.resident = (int)(grid / 8);
+    kern<<<dim3((unsigned)grid), dim3(kAttnThreads<D, BQ>), lds, st>>>(b);
     return hipGetLastError();
 }
 
