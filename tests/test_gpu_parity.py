@@ -314,6 +314,44 @@ def test_deterministic(dev, name):
     assert torch.equal(a, b)
 
 
+# --------------------------------------------------------------------------- many heads, every row
+# 96 queue positions per XCD: a third of the query blocks start their exact tiles at a nonzero
+# phase, the persistent workgroups run more than one block each and may take blocks from other
+# XCDs' queues; every output row is compared with the oracle.
+_many = {}
+
+
+def many_heads_inputs():
+    if not _many:
+        w = small_workload("many_heads", (16, 128), 128, 128, H=24, B=2, seed=31)
+        _many["w"] = w
+        _many["qkv"] = synth.make_qkv(w)
+    return _many["w"], _many["qkv"]
+
+
+@pytest.mark.parametrize("mode,beta", [("sparse", 0.5), ("sparse_no_correction", 0.8), ("dense", 0.0)])
+def test_forward_parity_many_heads(dev, mode, beta):
+    w, (q, k, v) = many_heads_inputs()
+    print(f"[parity] many heads B={w.B} H={w.H} N={w.N} mode={mode} beta={beta}", flush=True)
+    out, gmask, counts = run_gpu(dev, w, q, k, v, beta, mode)
+    qn, kn, vn = to_np(q), to_np(k), to_np(v)
+    ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode)
+    if mode != "dense":
+        flips = assert_mask_matches(gmask, ref["mask"], ref["s_hat"], ref["tau"])
+        if flips:
+            ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, mask=gmask)
+        assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
+    assert_output_close(to_np(out), ref["out"], w.dtype, f"many_heads/{mode}/{beta}")
+
+
+def test_many_heads_beta_minus_inf_is_bitwise_dense(dev):
+    w, (q, k, v) = many_heads_inputs()
+    dense, _, _ = run_gpu(dev, w, q, k, v, 0.0, "dense", want_mask=False)
+    out, gmask, _ = run_gpu(dev, w, q, k, v, -INF, "sparse")
+    assert gmask.all()
+    assert torch.equal(out, dense)
+
+
 # --------------------------------------------------------------------------- full workload shapes
 
 @pytest.fixture(scope="module", params=["video480p", "image", "video720p"])
