@@ -7,12 +7,13 @@
 //   3. moments        mean and centred covariance of the routable pooled keys, f64 sums
 //   4. tau            tau_i = mu_i + beta*sigma_i from the moments   (Eqs. threshold_routing,
 //                                                                       threshold_stats_exact)
-//   4b. order         sparse modes: order of each head's query blocks for the attention
-//                     grid (scheduling only: blocks with similar selections share an L2)
-//   5. routed_attn    one workgroup per (b, h, query block): routes every key block on chip
-//                     from f32 proxies, then runs one online-softmax pass over correction
-//                     tiles (pooled keys, Section 3.2 "Proxy-Score Reuse") and exact tiles
-//                     (selected key blocks), with bf16 MFMA for QK^T and f16 MFMA for PV
+//   4b. order         sparse modes: order of each head's query blocks in the attention
+//                     kernel's work queues (scheduling: blocks with similar selections share an L2)
+//   5. routed_attn    persistent workgroups claim (b, h, query block) items from per-XCD
+//                     queues; per block: route every key block on chip from f32 proxies, then
+//                     one online-softmax pass over correction tiles (pooled keys, Section 3.2
+//                     "Proxy-Score Reuse") and exact tiles (selected key blocks), with bf16
+//                     MFMA for QK^T and f16 MFMA for PV
 //   6. count_reduce   per-head number of selected routable pairs
 //
 // Tile math (wave64, v_mfma_f32_32x32x16_{bf16,f16}): each wave owns 32 query rows and

@@ -52,8 +52,8 @@ def run_gpu(dev, w, q, k, v, beta, mode, want_mask=True, threshold_mode="exact")
     mw = sb.mask_words(nkr)
     mask = torch.zeros((w.B, w.H, w.NQ, mw), dtype=torch.int32, device=dev) if want_mask else None
     counts = torch.full((w.B, w.H), -1, dtype=torch.int32, device=dev)
-    # NaN-filled output: every row must be written by exactly the workgroup of its query block
-    # (the sparse kernels visit query blocks in a data-dependent order)
+    # NaN-filled output: every row must be written by whichever workgroup claimed its query block
+    # (the kernels hand out query blocks through work queues, in a data-dependent order)
     out = torch.full_like(qd, math.nan)
     sb.forward(qd, kd, vd, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens, out=out,
                counts=counts, mask_out=mask, threshold_mode=threshold_mode)
