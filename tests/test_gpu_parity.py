@@ -352,6 +352,30 @@ def test_many_heads_beta_minus_inf_is_bitwise_dense(dev):
     assert torch.equal(out, dense)
 
 
+def test_concurrent_streams_own_workspaces(dev):
+    # Two forwards in flight at once on two streams, each with its own workspace (which holds the
+    # pre-pass results and the work-queue counters) and counts: both match the sequential results
+    # bit for bit.
+    w, (q, k, v) = many_heads_inputs()
+    qd, kd, vd = (t.to(dev) for t in (q, k, v))
+    ref_s = sb.forward(qd, kd, vd, w.block_q, 64, 0.5, "sparse")
+    ref_d = sb.forward(qd, kd, vd, w.block_q, 64, 0.0, "dense")
+    ws = [torch.empty(sb.workspace_bytes(w.B, w.H, w.N, w.d, w.block_q, 64, m, sb.SOL_BF16, 0), dtype=torch.uint8,
+                      device=dev) for m in ("sparse", "dense")]
+    counts = [torch.zeros((w.B, w.H), dtype=torch.int32, device=dev) for _ in range(2)]
+    outs = [torch.full_like(qd, math.nan) for _ in range(2)]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]   # default priority
+    torch.cuda.synchronize()
+    for _ in range(3):
+        with torch.cuda.stream(streams[0]):
+            sb.forward(qd, kd, vd, w.block_q, 64, 0.5, "sparse", out=outs[0], workspace=ws[0], counts=counts[0])
+        with torch.cuda.stream(streams[1]):
+            sb.forward(qd, kd, vd, w.block_q, 64, 0.0, "dense", out=outs[1], workspace=ws[1], counts=counts[1])
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], ref_s)
+    assert torch.equal(outs[1], ref_d)
+
+
 # --------------------------------------------------------------------------- full workload shapes
 
 @pytest.fixture(scope="module", params=["video480p", "image", "video720p"])
