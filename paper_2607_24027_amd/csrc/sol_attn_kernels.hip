@@ -832,6 +832,7 @@ struct AttnArgs {
     const uint16_t* order;        // [BH][NQ] query-block order (sparse modes), or null: identity
     uint32_t* queue;              // [8][32] per-XCD claim counters, zero at launch
     int resident;                 // workgroups per XCD in the persistent grid (grid / 8)
+    int hlog;                     // log2 of the heads whose blocks are in the queues at once (no causal mask)
     int BH, N, NQ, NK, NKr, NC, MW, per_x;
     float scale, c_log2;
     float bias_full, bias_last;   // log2(n_j)/c_log2 for full blocks and for the last block
@@ -1642,10 +1643,10 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
 
 // The fused kernel runs persistent workgroups (as many as fit on the device at once) that
 // claim query blocks from eight queues, one per XCD.  Queue x lists, in order, the blocks of
-// a fixed XCD-aware assignment: position y holds block y % per_x of XCD x's contiguous range
-// of head y / per_x (through the query-block order in the sparse modes), so the workgroups
-// resident on one XCD work through neighbouring blocks of one head and share its K/V in
-// their L2.  Under a causal mask the work of a query block grows with its index, so the
+// a fixed XCD-aware assignment: 2^hlog heads at a time, each on 8 >> hlog XCDs, and queue x
+// holds a contiguous range of per_x blocks of its head (through the query-block order in the
+// sparse modes), so the workgroups resident on one XCD work through neighbouring blocks of one
+// head and share its K/V in their L2.  Under a causal mask the work of a query block grows with its index, so the
 // head's blocks are cut into 16 segments and queue x takes segment 15 - x (descending, the
 // longer blocks first) and then segment x.  Consecutive workgroups go round-robin to the 8
 // XCDs, so workgroup w serves queue w & 7 first; once that queue is empty it takes blocks
@@ -1659,7 +1660,8 @@ void routed_attn_kernel(AttnArgs a) {
     extern __shared__ __attribute__((aligned(16))) char smem[];
     __shared__ int s_task[2];
     const int home = blockIdx.x & 7;
-    const unsigned qlen = (unsigned)a.per_x * (unsigned)a.BH;   // positions per queue
+    const unsigned groups = CAUSAL ? (unsigned)a.BH : (unsigned)((a.BH + (1 << a.hlog) - 1) >> a.hlog);
+    const unsigned qlen = (unsigned)a.per_x * groups;   // positions per queue
     for (;;) {
         __syncthreads();   // the previous block is done with LDS and with s_task
         // Claims are made when a block starts, not ahead of it: a queue position then also
@@ -1696,16 +1698,20 @@ void routed_attn_kernel(AttnArgs a) {
         __syncthreads();
         const int x = s_task[0], y = s_task[1];
         if (x < 0) return;
-        const int bh = y / a.per_x;
-        int qi;
+        int bh, qi;
         if constexpr (CAUSAL) {
+            bh = y / a.per_x;
             const int u = y % a.per_x, hp = a.per_x >> 1;
             qi = u < hp ? (15 - x) * hp + (hp - 1 - u) : x * hp + (u - hp);
         } else {
-            qi = x * a.per_x + (y % a.per_x);
-            if (a.order != nullptr && qi < a.NQ) qi = a.order[(size_t)bh * a.NQ + qi];
+            // 2^hlog heads at a time, each on 8 >> hlog XCDs: queue x serves head (x >> gl) of
+            // the current group, blocks (x mod 2^gl)*per_x ..
+            const int gl = 3 - a.hlog;
+            bh = ((y / a.per_x) << a.hlog) + (x >> gl);
+            qi = (x & ((1 << gl) - 1)) * a.per_x + (y % a.per_x);
+            if (a.order != nullptr && bh < a.BH && qi < a.NQ) qi = a.order[(size_t)bh * a.NQ + qi];
         }
-        if (qi < a.NQ) attn_block<D, BQ, MODE, CAUSAL>(a, smem, bh, qi, y);
+        if (bh < a.BH && qi < a.NQ) attn_block<D, BQ, MODE, CAUSAL>(a, smem, bh, qi, y);
     }
 }
 
@@ -1870,7 +1876,8 @@ hipError_t launch_attn_bf16(const Shape& s, const AttnArgs& a, hipStream_t st) {
     if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
     if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
     if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, kAttnThreads<D, BQ>, lds)) != hipSuccess) return e;
-    const long long positions = 8LL * a.per_x * a.BH;
+    const long long groups = CAUSAL ? a.BH : ((a.BH + (1 << a.hlog) - 1) >> a.hlog);
+    const long long positions = 8LL * a.per_x * groups;
     long long grid = ((long long)std::max(cus * std::max(occ, 1), 8) / 8) * 8;
     grid = std::min(grid, positions);
     AttnArgs b = a;
@@ -2028,6 +2035,20 @@ hipError_t launch_tau(const float* qbar, const float* muk, const float* cov, flo
     return hipGetLastError();
 }
 
+// Heads whose query blocks are in the attention kernel's queues at once (log2).  The workgroups
+// resident on one XCD share its L2, so each XCD should work through one head at a time; with
+// all 8 XCDs on one head each gets only NQ/8 blocks of it.  Fewer XCDs per head give each XCD
+// longer runs of one head, as far as the heads in flight keep their K/V tiles (bf16 K and f16
+// V^T, 4*Npad*d bytes per head) within kMallBudget of the shared MALL.  Heads differ in their
+// kept fraction, so the XCDs of one head may finish early; the queues' stealing evens that out.
+constexpr double kMallBudget = 96.0 * 1024 * 1024;
+int heads_in_flight_log2(const Shape& s) {
+    const double kv = 4.0 * (double)s.Npad * s.d;
+    int hl = 0;
+    while (hl < 3 && (double)(2 << hl) * kv <= kMallBudget && (2 << hl) <= s.BH) ++hl;
+    return hl;
+}
+
 hipError_t launch_forward(const Shape& s, const void* q, const void* k, const void* v, void* out, float beta,
                           const Workspace& ws, uint32_t* counts, uint32_t* mask_out, hipStream_t st,
                           hipEvent_t ev_start, hipEvent_t ev_stop) {
@@ -2074,7 +2095,8 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
         a.blkcount = ws.blkcount;
         a.mask_out = mask_out;
         a.BH = s.BH; a.N = s.N; a.NQ = s.NQ; a.NK = s.NK; a.NKr = s.NKr; a.NC = s.NC; a.MW = s.MW;
-        a.per_x = s.causal ? 2 * ((s.NQ + 15) / 16) : (s.NQ + 7) / 8;
+        a.hlog = s.causal ? 0 : heads_in_flight_log2(s);
+        a.per_x = s.causal ? 2 * ((s.NQ + 15) / 16) : (s.NQ + (8 >> a.hlog) - 1) / (8 >> a.hlog);
         a.scale = scale;
         a.causal_g = s.causal;
         a.beta = beta;
