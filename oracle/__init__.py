@@ -5,7 +5,7 @@ TEST INFRASTRUCTURE: only ``tests/``, ``__graft_entry__.smoke()`` and the
 GPU library in ``paper_2607_24027_amd``.
 """
 from .sol_attn_oracle import (  # noqa: F401
-    BAND, MODES, approx_terms, block_counts, diagonal_sigma, exact_terms, forward,
-    frac_selected, pool_means, proxy_scores, route, routing, row_stats,
+    BAND, MODES, approx_terms, block_counts, diagonal_sigma, exact_logits, exact_terms, forward,
+    pool_means, proxy_scores, route, routing, row_stats,
     row_stats_from_moments, thresholds,
 )

@@ -207,11 +207,23 @@ def route_topp(s_hat: np.ndarray, p: float) -> np.ndarray:
 # Combined softmax terms (Section 3.2, Eqs. solattn_denominator / numerator)
 # ---------------------------------------------------------------------------
 
-def exact_terms(q_rows, keys, values, scale, shift, visible=None):
+def exact_logits(q_rows, keys, scale, visible=None):
+    """Exact logits scale * q.k_u of each row against a set of keys, -inf where the row does not
+    see the key (``visible`` [rows, keys], causal masks)."""
+    lg = scale * (q_rows @ keys.T)
+    if visible is not None:
+        lg = np.where(visible, lg, -np.inf)
+    return lg
+
+
+def exact_terms(q_rows, keys, values, scale, shift, visible=None, logits=None):
     """Exact-branch contributions of a set of keys to each row:
     D = sum_u exp(scale q.k_u - shift),  N = sum_u exp(scale q.k_u - shift) v_u,
-    the sums running over the keys a row sees (``visible`` [rows, keys], causal masks)."""
-    w = np.exp(scale * (q_rows @ keys.T) - shift[:, None])
+    the sums running over the keys a row sees (``visible`` [rows, keys], causal masks).
+    ``logits``: the same rows' exact_logits(q_rows, keys, scale, visible), if already formed."""
+    if logits is None:
+        logits = exact_logits(q_rows, keys, scale, visible)
+    w = np.exp(logits - shift[:, None])
     if visible is not None:
         w = np.where(visible, w, 0.0)
     return w.sum(axis=1), w @ values
@@ -275,10 +287,9 @@ def _forward_head(args):
         ab = np.asarray(approx_blocks, dtype=np.int64)
         # Row shift for overflow safety: the largest exponent of any term.
         cand = []
+        lg = None
         if key_idx.size:
-            lg = scale * (q_rows @ kh[key_idx].T)
-            if visible is not None:
-                lg = np.where(visible, lg, -np.inf)
+            lg = exact_logits(q_rows, kh[key_idx], scale, visible)
             cand.append(lg.max(axis=1))
         if ab.size:
             cand.append((scale * (q_rows @ kbar[ab].T) + np.log(kcounts[ab])).max(axis=1))
@@ -291,7 +302,7 @@ def _forward_head(args):
         den = np.zeros(r1 - r0)
         num = np.zeros((r1 - r0, d))
         if key_idx.size:
-            dd, nn = exact_terms(q_rows, kh[key_idx], vh[key_idx], scale, shift, visible)
+            dd, nn = exact_terms(q_rows, None, vh[key_idx], scale, shift, visible, logits=lg)
             den += dd
             num += nn
         if ab.size:
@@ -415,7 +426,3 @@ def routing(q, k, block_q: int, block_k: int, beta: float, keep_tail_tokens: int
             "frac": sel.sum(axis=(-1, -2)) / n_routable, "band": band, "qbar": qbar, "kbar": kbar,
             "routable": routable}
 
-
-def frac_selected(mask: np.ndarray) -> np.ndarray:
-    """Per-(b,h) fraction of routable (query block, key block) pairs selected."""
-    return mask.mean(axis=(-1, -2))
