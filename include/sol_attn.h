@@ -16,9 +16,17 @@
  * N >= 1 with ragged last blocks (a block's statistics use only its valid
  * tokens); bf16 inputs (the hot path) and f32 inputs (a correctness-first
  * path).  The softmax scale is 1/sqrt(d) for the exact logits and the
- * proxies alike.  bf16 value inputs must lie within the f16 range
- * (|v| <= 65504): the value operand of the probability-times-value products
- * is carried in f16.
+ * proxies alike.
+ *
+ * Range contract of the bf16 path (checked by nobody: outside it results are
+ * undefined, typically inf/NaN, and no error code is returned):
+ *   - v: every element within the f16 range (|v| <= 65504), in every mode: the
+ *     value operand of the probability-times-value products is carried in f16;
+ *   - q and k, in SOL_SPARSE only: every element of q and every block mean of k
+ *     within the f16 range: the correction tiles multiply an f16 copy of the
+ *     query rows by f16 copies of the pooled keys.
+ * bf16 itself reaches 3.4e38, so these are real restrictions; attention inputs
+ * of transformer layers sit far inside them.
  */
 #ifndef SOL_ATTN_H
 #define SOL_ATTN_H
@@ -56,7 +64,7 @@ enum {
     SOL_ERR_UNSUPPORTED = -2,  /* valid but unsupported shape (d, block sizes, too many blocks) */
     SOL_ERR_HIP = -3,          /* a HIP runtime call failed (allocation, launch, sync) */
     SOL_ERR_WORKSPACE = -4,    /* caller workspace smaller than sol_attn_workspace_bytes() */
-    SOL_ERR_NO_DATA = -5       /* sol_attn_stats before any forward, or B/H mismatch */
+    SOL_ERR_NO_DATA = -5       /* sol_attn_stats: no forward wrote those counts, or B/H mismatch */
 };
 
 /*
@@ -98,10 +106,10 @@ int sol_attn_thresholds(const float* qbar, const float* kbar,
                         float beta, int threshold_mode, void* stream);
 
 /*
- * Baseline routing with a materialised proxy map (Section 2, after Eq. block_proxy:
- * "standard routing applies top-k to s_hat_i or top-p to p_hat_i"), provided to measure
- * what the on-the-fly threshold routing of the forward calls avoids; the forward never
- * uses it.
+ * Baseline routing with a materialised proxy map: the top-k and top-p selection rules
+ * that Section 2 describes over the proxy row s_hat_i of Eq. block_proxy and its softmax
+ * p_hat_i.  Provided to measure what the on-the-fly threshold routing of the forward
+ * calls avoids; the forward never uses it.
  *
  * Writes proxies[b,h,i,j] = s * Qbar_i . Kbar_j (s = 1/sqrt(d)) for the first nk_routable
  * key blocks, then selects per query block:
@@ -212,12 +220,26 @@ size_t sol_attn_workspace_bytes(int B, int H, int N, int d, int block_q, int blo
                                 int mode, int dtype, int keep_tail_tokens);
 
 /*
- * Per-head selected-block fraction of the most recent forward call in this
- * process: frac_per_head[b*H+h] = counts[b*H+h] / (NQ * NKr) (host float array
- * of B*H entries).  Synchronises that call's stream.  Returns SOL_ERR_NO_DATA
- * if there was no forward or B/H differ from it.
+ * Per-head selected-block fraction of a forward call (the per-head sparsity
+ * counter): frac_per_head[b*H+h] = counts[b*H+h] / (routable pairs of one head),
+ * NQ * NKr without a mask (host float array of B*H entries, written).
+ *
+ * counts: the [B,H] u32 device buffer a forward call of this library wrote
+ *   (the `counts` argument of sol_attn_forward_ex / sol_attn_forward_causal),
+ *   or NULL for the library's own counts buffer as written by the last forward
+ *   on the calling thread that passed counts = NULL (sol_attn_forward always
+ *   does).  The library remembers, per counts buffer, the shape of the forward
+ *   that last wrote it, so two forwards in flight on two streams with their own
+ *   counts buffers each keep their own statistics.  A caller-owned buffer must
+ *   still be allocated when this is called.
+ * Waits for the forward that last wrote the buffer (an event recorded on its
+ * stream, so the stream itself may have been destroyed since), then copies the
+ * counts to the host.  Returns SOL_ERR_NO_DATA if the buffer was not written by
+ * a forward of this library, if counts is NULL and the last forward on this
+ * thread used a caller-owned buffer (or there was none), or if B/H differ from
+ * that forward's.
  */
-int sol_attn_stats(float* frac_per_head, int B, int H);
+int sol_attn_stats(float* frac_per_head, int B, int H, const uint32_t* counts);
 
 /*
  * Kernel timing (profiling aid).  While enabled, every forward records a pair

@@ -31,7 +31,7 @@ SIGNATURES = {
     "sol_attn_forward_ex": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _I, _I, _P, _S, _P, _P, _P]),
     "sol_attn_forward_causal": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _I, _I, _P, _S, _P, _P, _P]),
     "sol_attn_workspace_bytes": (_S, [_I, _I, _I, _I, _I, _I, _I, _I, _I]),
-    "sol_attn_stats": (_I, [_P, _I, _I]),
+    "sol_attn_stats": (_I, [_P, _I, _I, _P]),
     "sol_attn_timing_enable": (_I, [_I]),
     "sol_attn_kernel_timing": (_I, [_P, _P]),
     "sol_attn_route_materialized": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _I, _F, _P]),
@@ -91,11 +91,68 @@ def _dtype_code(t) -> int:
 
 
 def _check_qkv(*ts):
-    for t in ts:
-        if t is None:
-            continue
-        if not t.is_cuda or not t.is_contiguous() or t.dim() != 4:
-            raise ValueError("tensors must be contiguous 4-D [B,H,N,d] device tensors")
+    """q, k, v (any may be None): contiguous 4-D tensors of one shape, dtype and GPU device."""
+    present = [t for t in ts if t is not None]
+    if not present:
+        raise ValueError("no input tensors given")
+    ref = present[0]
+    for t in present:
+        if t.dim() != 4 or not t.is_contiguous():
+            raise ValueError("q, k and v must be contiguous 4-D [B,H,N,d] tensors")
+        if tuple(t.shape) != tuple(ref.shape):
+            raise ValueError(f"q, k and v must have one shape (got {tuple(ref.shape)} and {tuple(t.shape)})")
+        if t.dtype != ref.dtype:
+            raise ValueError(f"q, k and v must have one dtype (got {ref.dtype} and {t.dtype})")
+        if t.device != ref.device:
+            raise ValueError(f"q, k and v must be on one device (got {ref.device} and {t.device})")
+    _dtype_code(ref)
+
+
+def _require_gpu(t):
+    if t.device.type != "cuda":
+        raise ValueError(f"tensors must be on a GPU (got device {t.device})")
+
+
+def _check_buffer(name, t, shape, dtypes, device):
+    """An output/scratch tensor handed to the library: exact shape, dtype and device, contiguous."""
+    if t is None:
+        return
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)} (got {tuple(t.shape)})")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name} must have dtype {' or '.join(str(d) for d in dtypes)} (got {t.dtype})")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device} (got {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _check_forward_buffers(q, block_q, nkr, out=None, counts=None, mask_out=None, workspace=None):
+    """out like q; counts [B,H] 32-bit ints; mask_out [B,H,NQ,ceil(NKr/32)] int32; workspace a 1-D
+    uint8 tensor (its size is checked by the library against sol_attn_workspace_bytes)."""
+    import torch
+    B, H, N, d = q.shape
+    _check_buffer("out", out, q.shape, (q.dtype,), q.device)
+    int32_like = tuple({torch.int32, getattr(torch, "uint32", torch.int32)})
+    _check_buffer("counts", counts, (B, H), int32_like, q.device)
+    if block_q > 0:
+        _check_buffer("mask_out", mask_out, (B, H, -(-N // block_q), mask_words(nkr)), (torch.int32,), q.device)
+    if workspace is not None:
+        if workspace.dim() != 1:
+            raise ValueError("workspace must be a 1-D uint8 tensor")
+        _check_buffer("workspace", workspace, workspace.shape, (torch.uint8,), q.device)
+
+
+def _check_pooled(qbar, kbar):
+    """Pooled queries [B,H,NQ,d] and keys [B,H,NK,d]: f32, same B, H, d and GPU device."""
+    import torch
+    for name, t in (("qbar", qbar), ("kbar", kbar)):
+        if t.dim() != 4 or t.dtype != torch.float32:
+            raise ValueError(f"{name} must be a 4-D float32 tensor")
+    if qbar.shape[:2] != kbar.shape[:2] or qbar.shape[3] != kbar.shape[3]:
+        raise ValueError(f"qbar {tuple(qbar.shape)} and kbar {tuple(kbar.shape)} disagree in B, H or d")
+    if qbar.device != kbar.device:
+        raise ValueError("qbar and kbar must be on one device")
 
 
 def pool_blocks(q, k, v, block_q: int, block_k: int):
@@ -103,6 +160,9 @@ def pool_blocks(q, k, v, block_q: int, block_k: int):
     import torch
     _check_qkv(q, k, v)
     B, H, N, d = q.shape
+    if block_q <= 0 or block_k <= 0:
+        raise ValueError("block sizes must be positive")
+    _require_gpu(next(t for t in (q, k, v) if t is not None))
     nq, nk = -(-N // block_q), -(-N // block_k)
     qbar = torch.empty((B, H, nq, d), device=q.device, dtype=torch.float32)
     kbar = torch.empty((B, H, nk, d), device=q.device, dtype=torch.float32)
@@ -116,9 +176,11 @@ def thresholds(qbar, kbar, beta: float, nk_routable: Optional[int] = None, thres
     """(tau, mu, sigma) [B,H,NQ] f32 from pooled queries/keys (moment form, or the
     diagonal estimator with threshold_mode="diagonal")."""
     import torch
+    _check_pooled(qbar, kbar)
     B, H, NQ, d = qbar.shape
     NK = kbar.shape[2]
     nkr = NK if nk_routable is None else nk_routable
+    _require_gpu(qbar)
     tau = torch.empty((B, H, NQ), device=qbar.device, dtype=torch.float32)
     mu = torch.empty_like(tau)
     sigma = torch.empty_like(tau)
@@ -140,9 +202,13 @@ def route_materialized(qbar, kbar, rule: str, param: float, nk_routable: Optiona
     """Baseline routing through a materialised proxy map: rule "topk" (param = k) or "topp"
     (param = p).  Returns (proxies [B,H,NQ,NKr] f32, mask [B,H,NQ,MW] int32) device tensors."""
     import torch
+    _check_pooled(qbar, kbar)
     B, H, NQ, d = qbar.shape
     NK = kbar.shape[2]
     nkr = NK if nk_routable is None else nk_routable
+    _check_buffer("proxies", proxies, (B, H, NQ, nkr), (torch.float32,), qbar.device)
+    _check_buffer("mask_out", mask_out, (B, H, NQ, mask_words(nkr)), (torch.int32,), qbar.device)
+    _require_gpu(qbar)
     if proxies is None:
         proxies = torch.empty((B, H, NQ, nkr), device=qbar.device, dtype=torch.float32)
     if mask_out is None:
@@ -164,10 +230,13 @@ def forward(q, k, v, block_q: int, block_k: int, tau: float, mode="sparse", keep
             causal_granule: int = 0):
     """Routed attention forward through sol_attn_forward_ex, or sol_attn_forward_causal when
     causal_granule > 0.  Returns out.  threshold_mode "diagonal" ORs SOL_THRESHOLD_DIAGONAL
-    into the mode."""
+    into the mode.  Every tensor is checked for shape, dtype and device before the call."""
     import torch
     _check_qkv(q, k, v)
     B, H, N, d = q.shape
+    nkr = -(-N // block_k) - keep_tail_tokens // block_k if block_k > 0 else 0
+    _check_forward_buffers(q, block_q, nkr, out, counts, mask_out, workspace)
+    _require_gpu(q)
     if out is None:
         out = torch.empty_like(q)
     m = _mode_code(mode, threshold_mode)
@@ -187,6 +256,14 @@ def forward(q, k, v, block_q: int, block_k: int, tau: float, mode="sparse", keep
 
 def forward_short(q, k, v, out, block_q: int, block_k: int, tau: float, mode="sparse"):
     """The 12-argument sol_attn_forward (bf16, default stream, library workspace)."""
+    import torch
+    _check_qkv(q, k, v)
+    if q.dtype != torch.bfloat16:
+        raise ValueError("sol_attn_forward takes bf16 tensors")
+    if out is None:
+        raise ValueError("out must be given")
+    _check_forward_buffers(q, block_q, 0, out)
+    _require_gpu(q)
     B, H, N, d = q.shape
     m = MODES[mode] if isinstance(mode, str) else int(mode)
     _check(lib().sol_attn_forward(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, block_q, block_k,
@@ -194,10 +271,17 @@ def forward_short(q, k, v, out, block_q: int, block_k: int, tau: float, mode="sp
     return out
 
 
-def stats(B: int, H: int):
-    """Per-head selected fraction of the last forward (host list, synchronising)."""
+def stats(B: int, H: int, counts=None):
+    """Per-head selected fraction (host list, synchronising) of the forward that wrote `counts`
+    (a [B,H] device tensor passed to forward()), or with counts=None of the last forward on this
+    thread that used the library's own counts buffer."""
+    if counts is not None:
+        _check_buffer("counts", counts, (B, H), (counts.dtype,), counts.device)
+        if counts.element_size() != 4 or counts.dtype.is_floating_point:
+            raise ValueError("counts must be a 32-bit integer tensor")
+        _require_gpu(counts)
     arr = (ctypes.c_float * (B * H))()
-    _check(lib().sol_attn_stats(ctypes.cast(arr, ctypes.c_void_p), B, H))
+    _check(lib().sol_attn_stats(ctypes.cast(arr, ctypes.c_void_p), B, H, _ptr(counts)))
     return [float(x) for x in arr]
 
 

@@ -47,16 +47,27 @@ struct DeviceBuffers {
 std::mutex g_mu;
 std::map<int, DeviceBuffers> g_bufs;
 
-// Record of the most recent forward, for sol_attn_stats.
-struct LastCall {
-    bool valid = false;
+// What sol_attn_stats needs to turn a counts buffer into fractions: one record per counts
+// buffer a forward wrote (keyed by its device address), with an event recorded on the
+// forward's stream right after the counts were written.  Waiting on the event instead of the
+// stream keeps the record valid after the caller destroys the stream.  Records are recycled
+// first-in first-out beyond kMaxRecords buffers; their events are reused, never destroyed
+// before sol_attn_release.
+struct CountsRecord {
     int device = 0;
     int B = 0, H = 0;
     double routable_pairs = 0.0;   // (query block, routable key block) pairs of one head
-    const uint32_t* counts = nullptr;
-    hipStream_t stream = nullptr;
+    hipEvent_t done = nullptr;     // recorded on the forward's stream after its counts
+    bool library = false;          // the library's own counts buffer (counts == NULL)
 };
-LastCall g_last;
+constexpr size_t kMaxRecords = 1024;
+std::map<const uint32_t*, CountsRecord> g_records;
+std::vector<const uint32_t*> g_record_order;        // insertion order, for recycling
+std::map<int, std::vector<hipEvent_t>> g_free_events;  // per device: events of recycled records
+std::map<int, std::vector<hipEvent_t>> g_all_events;   // per device: every event created
+
+// The counts buffer of the last forward on this thread, for sol_attn_stats(..., NULL).
+thread_local const uint32_t* t_last_counts = nullptr;
 
 // Kernel timing: event pairs recorded around the fused attention kernel.
 constexpr int kMaxTimed = 4096;
@@ -211,6 +222,49 @@ double routable_pairs(const sol::Shape& s) {
     return tot;
 }
 
+// Forgets the record of a counts buffer (its event goes back to its device's pool).  Caller
+// holds g_mu.
+void drop_record(const uint32_t* counts) {
+    auto it = g_records.find(counts);
+    if (it == g_records.end()) return;
+    g_free_events[it->second.device].push_back(it->second.done);
+    g_records.erase(it);
+    auto pos = std::find(g_record_order.begin(), g_record_order.end(), counts);
+    if (pos != g_record_order.end()) g_record_order.erase(pos);
+}
+
+// Creates or updates the record of a counts buffer and records its event on `st`.  Caller
+// holds g_mu; device `dev` is current.
+hipError_t note_counts(int dev, const uint32_t* counts, int B, int H, double pairs, bool library, hipStream_t st) {
+    auto it = g_records.find(counts);
+    if (it != g_records.end() && it->second.device != dev) {   // same address, another device's buffer
+        drop_record(counts);
+        it = g_records.end();
+    }
+    if (it == g_records.end()) {
+        while (g_records.size() >= kMaxRecords && !g_record_order.empty()) drop_record(g_record_order.front());
+        CountsRecord r;
+        r.device = dev;
+        auto& pool = g_free_events[dev];
+        if (!pool.empty()) {
+            r.done = pool.back();
+            pool.pop_back();
+        } else {
+            hipError_t e = hipEventCreateWithFlags(&r.done, hipEventDisableTiming);
+            if (e != hipSuccess) return e;
+            g_all_events[dev].push_back(r.done);
+        }
+        it = g_records.emplace(counts, r).first;
+        g_record_order.push_back(counts);
+    }
+    CountsRecord& r = it->second;
+    r.B = B;
+    r.H = H;
+    r.routable_pairs = pairs;
+    r.library = library;
+    return hipEventRecord(r.done, st);
+}
+
 int forward_impl(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d, int block_q,
                  int block_k, float tau, int mode, int dtype, int keep_tail_tokens, int causal_granule,
                  void* workspace, size_t workspace_bytes, uint32_t* counts, uint32_t* mask_out, void* stream) {
@@ -249,6 +303,7 @@ int forward_impl(const void* q, const void* k, const void* v, void* out, int B, 
             if (db.counts) {
                 e = hipDeviceSynchronize();
                 if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+                drop_record(db.counts);
                 (void)hipFree(db.counts);
                 db.counts = nullptr;
                 db.counts_n = 0;
@@ -269,13 +324,10 @@ int forward_impl(const void* q, const void* k, const void* v, void* out, int B, 
     }
     e = sol::launch_forward(s, q, k, v, out, tau, ws, counts, mask_out, st, ev0, ev1);
     if (e != hipSuccess) return hip_fail(e, "forward launch");
-    g_last.valid = true;
-    g_last.device = dev;
-    g_last.B = B;
-    g_last.H = H;
-    g_last.routable_pairs = routable_pairs(s);
-    g_last.counts = counts;
-    g_last.stream = st;
+    // Record where these counts came from, and when they are complete (caller holds g_mu).
+    e = note_counts(dev, counts, B, H, routable_pairs(s), counts == db.counts, st);
+    if (e != hipSuccess) return hip_fail(e, "recording the counts event");
+    t_last_counts = counts;
     return ok();
 }
 
@@ -306,32 +358,41 @@ int sol_attn_forward(const void* q, const void* k, const void* v, void* out, int
                                nullptr, nullptr);
 }
 
-int sol_attn_stats(float* frac_per_head, int B, int H) {
+int sol_attn_stats(float* frac_per_head, int B, int H, const uint32_t* counts) {
     if (!frac_per_head) return fail(SOL_ERR_INVALID_ARG, "frac_per_head must be non-null");
-    LastCall last;
+    if (B <= 0 || H <= 0) return fail(SOL_ERR_INVALID_ARG, "B and H must be positive (got %d, %d)", B, H);
+    CountsRecord rec;
+    const uint32_t* buf = counts;
     {
         std::lock_guard<std::mutex> lock(g_mu);
-        last = g_last;
+        if (!buf) {
+            buf = t_last_counts;
+            if (!buf) return fail(SOL_ERR_NO_DATA, "no forward call has been made on this thread");
+        }
+        auto it = g_records.find(buf);
+        if (it == g_records.end())
+            return fail(SOL_ERR_NO_DATA, counts ? "these counts were not written by a forward call of this library"
+                                                : "no forward call has been made on this thread");
+        rec = it->second;
+        if (!counts && !rec.library)
+            return fail(SOL_ERR_NO_DATA,
+                        "the last forward on this thread wrote caller-owned counts: pass that buffer as `counts`");
     }
-    if (!last.valid) return fail(SOL_ERR_NO_DATA, "no forward call has been made");
-    if (last.B != B || last.H != H)
-        return fail(SOL_ERR_NO_DATA, "B/H (%d, %d) differ from the last forward (%d, %d)", B, H, last.B, last.H);
+    if (rec.B != B || rec.H != H)
+        return fail(SOL_ERR_NO_DATA, "B/H (%d, %d) differ from the forward that wrote these counts (%d, %d)", B, H,
+                    rec.B, rec.H);
     int cur = 0;
     hipError_t e = hipGetDevice(&cur);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    if (cur != last.device && (e = hipSetDevice(last.device)) != hipSuccess) return hip_fail(e, "hipSetDevice");
+    if (cur != rec.device && (e = hipSetDevice(rec.device)) != hipSuccess) return hip_fail(e, "hipSetDevice");
     const size_t n = (size_t)B * H;
-    uint32_t* host = new uint32_t[n];
-    e = hipStreamSynchronize(last.stream);
-    if (e == hipSuccess) e = hipMemcpy(host, last.counts, n * sizeof(uint32_t), hipMemcpyDeviceToHost);
-    if (cur != last.device) (void)hipSetDevice(cur);
-    if (e != hipSuccess) {
-        delete[] host;
-        return hip_fail(e, "reading counts");
-    }
-    const double denom = last.routable_pairs > 0.0 ? last.routable_pairs : 1.0;
+    std::vector<uint32_t> host(n);
+    e = hipEventSynchronize(rec.done);
+    if (e == hipSuccess) e = hipMemcpy(host.data(), buf, n * sizeof(uint32_t), hipMemcpyDeviceToHost);
+    if (cur != rec.device) (void)hipSetDevice(cur);
+    if (e != hipSuccess) return hip_fail(e, "reading counts");
+    const double denom = rec.routable_pairs > 0.0 ? rec.routable_pairs : 1.0;
     for (size_t i = 0; i < n; ++i) frac_per_head[i] = (float)((double)host[i] / denom);
-    delete[] host;
     return ok();
 }
 
@@ -386,7 +447,16 @@ int sol_attn_release(void) {
     }
     (void)hipSetDevice(cur);
     g_bufs.clear();
-    g_last = LastCall{};
+    for (auto& kv : g_all_events) {
+        (void)hipSetDevice(kv.first);
+        for (hipEvent_t ev : kv.second) (void)hipEventDestroy(ev);
+    }
+    (void)hipSetDevice(cur);
+    g_all_events.clear();
+    g_free_events.clear();
+    g_records.clear();
+    g_record_order.clear();
+    t_last_counts = nullptr;
     return ok();
 }
 

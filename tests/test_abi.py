@@ -116,8 +116,117 @@ def test_other_entry_points_validate():
     assert rm(FAKE[0], FAKE[1], FAKE[2], FAKE[3], 1, 1, 4, 5000, 5000, 64, 1, 0.5, None) == sb.SOL_ERR_UNSUPPORTED
     assert rm(FAKE[0], FAKE[1], FAKE[2], FAKE[3], 1, 1, 4, 8, 8, 80, 0, 2.0, None) == sb.SOL_ERR_UNSUPPORTED
     arr = (ctypes.c_float * 4)()
-    assert lib.sol_attn_stats(ctypes.cast(arr, P), 2, 2) == sb.SOL_ERR_NO_DATA
-    assert lib.sol_attn_stats(None, 2, 2) == sb.SOL_ERR_INVALID_ARG
+    assert lib.sol_attn_stats(None, 2, 2, None) == sb.SOL_ERR_INVALID_ARG
+    assert lib.sol_attn_stats(ctypes.cast(arr, P), 0, 2, None) == sb.SOL_ERR_INVALID_ARG
+
+
+def test_stats_without_a_forward_has_no_data():
+    # No forward has run on this thread (CPU tests never launch one): with counts = NULL there
+    # is no record; a counts buffer no forward wrote has none either.  Both fail before any HIP
+    # call.
+    import threading
+    lib = sb.lib()
+    arr = (ctypes.c_float * 4)()
+    res = {}
+
+    def probe():
+        res["null"] = lib.sol_attn_stats(ctypes.cast(arr, P), 2, 2, None)
+        res["null_msg"] = sb.last_error()
+        res["foreign"] = lib.sol_attn_stats(ctypes.cast(arr, P), 2, 2, P(0x5000))
+        res["foreign_msg"] = sb.last_error()
+
+    t = threading.Thread(target=probe)   # a fresh thread: no last forward of its own
+    t.start()
+    t.join()
+    assert res["null"] == sb.SOL_ERR_NO_DATA and "thread" in res["null_msg"]
+    assert res["foreign"] == sb.SOL_ERR_NO_DATA and "not written" in res["foreign_msg"]
+
+
+# --------------------------------------------------------------------------- binding argument checks
+# The Python binding checks every tensor it hands to the library (shape, dtype, device, layout)
+# before the call, so a mismatched tensor never reaches a kernel.  CPU tensors get through the
+# shape/dtype/buffer checks and stop at the GPU check, which comes last.
+
+def _qkv(B=1, H=2, N=300, d=64, dtype=None):
+    import torch
+    dtype = dtype or torch.bfloat16
+    return tuple(torch.zeros((B, H, N, d), dtype=dtype) for _ in range(3))
+
+
+def test_binding_rejects_mismatched_inputs():
+    import torch
+    q, k, v = _qkv()
+    with pytest.raises(ValueError, match="one shape"):
+        sb.forward(q, k[:, :, :299].contiguous(), v, 64, 64, 0.5)
+    with pytest.raises(ValueError, match="one shape"):
+        sb.forward(q, k, torch.zeros((1, 2, 300, 128), dtype=torch.bfloat16), 64, 64, 0.5)
+    with pytest.raises(ValueError, match="one dtype"):
+        sb.forward(q, k.float(), v, 64, 64, 0.5)
+    with pytest.raises(ValueError, match="one device"):
+        sb.forward(q, k, torch.empty_like(v, device="meta"), 64, 64, 0.5)
+    with pytest.raises(ValueError, match="contiguous"):
+        sb.forward(q, k.transpose(2, 3).contiguous().transpose(2, 3), v, 64, 64, 0.5)
+    with pytest.raises(TypeError):
+        sb.forward(*(t.half() for t in (q, k, v)), 64, 64, 0.5)
+    with pytest.raises(ValueError, match="GPU"):
+        sb.forward(q, k, v, 64, 64, 0.5)   # every check passes but the device
+
+
+@pytest.mark.parametrize("what,bad", [
+    ("out", lambda q: torch_zeros((1, 2, 299, 64), "bfloat16")),
+    ("out", lambda q: torch_zeros((1, 2, 300, 64), "float32")),
+    ("out", lambda q: torch_zeros((1, 2, 300, 64), "bfloat16", device="meta")),
+    ("counts", lambda q: torch_zeros((2, 1), "int32")),
+    ("counts", lambda q: torch_zeros((1, 2), "int64")),
+    ("counts", lambda q: torch_zeros((1, 2), "float32")),
+    ("mask_out", lambda q: torch_zeros((1, 2, 5, 2), "int32")),     # 300 rows: NQ = NK = 5, one mask word
+    ("mask_out", lambda q: torch_zeros((1, 2, 4, 1), "int32")),
+    ("mask_out", lambda q: torch_zeros((1, 2, 5, 1), "int64")),
+    ("workspace", lambda q: torch_zeros((16,), "int32")),
+    ("workspace", lambda q: torch_zeros((4, 4), "uint8")),
+])
+def test_binding_rejects_bad_buffers(what, bad):
+    q, k, v = _qkv()
+    with pytest.raises(ValueError, match=what):
+        sb.forward(q, k, v, 64, 64, 0.5, **{what: bad(q)})
+
+
+def test_binding_accepts_matching_buffers_up_to_the_gpu_check():
+    q, k, v = _qkv()
+    bufs = dict(out=torch_zeros((1, 2, 300, 64), "bfloat16"), counts=torch_zeros((1, 2), "int32"),
+                mask_out=torch_zeros((1, 2, 5, 1), "int32"), workspace=torch_zeros((1024,), "uint8"))
+    with pytest.raises(ValueError, match="GPU"):
+        sb.forward(q, k, v, 64, 64, 0.5, **bufs)
+    # 64 forced tail tokens leave 4 routable key blocks: still one mask word
+    with pytest.raises(ValueError, match="GPU"):
+        sb.forward(q, k, v, 64, 64, 0.5, keep_tail_tokens=64, **bufs)
+
+
+def test_binding_short_form_and_other_calls_check_arguments():
+    import torch
+    q, k, v = _qkv()
+    with pytest.raises(ValueError, match="bf16"):
+        sb.forward_short(q.float(), k.float(), v.float(), torch.zeros_like(q.float()), 64, 64, 0.5)
+    with pytest.raises(ValueError, match="out"):
+        sb.forward_short(q, k, v, torch_zeros((1, 2, 300, 32), "bfloat16"), 64, 64, 0.5)
+    with pytest.raises(ValueError, match="one shape"):
+        sb.pool_blocks(q, k[:, :1].contiguous(), v, 64, 64)
+    with pytest.raises(ValueError, match="counts"):
+        sb.stats(1, 2, counts=torch_zeros((2, 2), "int32"))
+    with pytest.raises(ValueError, match="32-bit"):
+        sb.stats(1, 2, counts=torch_zeros((1, 2), "int64"))
+    qbar, kbar = torch_zeros((1, 2, 5, 64), "float32"), torch_zeros((1, 2, 5, 64), "float32")
+    with pytest.raises(ValueError, match="disagree"):
+        sb.thresholds(qbar, torch_zeros((1, 3, 5, 64), "float32"), 0.5)
+    with pytest.raises(ValueError, match="float32"):
+        sb.route_materialized(qbar.double(), kbar, "topk", 2)
+    with pytest.raises(ValueError, match="proxies"):
+        sb.route_materialized(qbar, kbar, "topk", 2, proxies=torch_zeros((1, 2, 5, 4), "float32"))
+
+
+def torch_zeros(shape, dtype, device="cpu"):
+    import torch
+    return torch.zeros(shape, dtype=getattr(torch, dtype), device=device)
 
 
 def test_workspace_bytes_accepts_the_threshold_flag():

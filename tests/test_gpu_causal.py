@@ -50,12 +50,16 @@ def routable_pairs(w, g):
     return int(r.sum())
 
 
+_last_counts = {}   # device counts of the last run_causal call, for sol_attn_stats
+
+
 def run_causal(dev, w, g, q, k, v, beta, mode):
     qd, kd, vd = (t.to(dev) for t in (q, k, v))
     mask = torch.zeros((w.B, w.H, w.NQ, sb.mask_words(w.NK)), dtype=torch.int32, device=dev)
     counts = torch.full((w.B, w.H), -1, dtype=torch.int32, device=dev)
     out = sb.forward(qd, kd, vd, w.block_q, 64, beta, mode, counts=counts, mask_out=mask, causal_granule=g)
     torch.cuda.synchronize()
+    _last_counts["t"] = counts
     gmask = sb.unpack_mask(mask.cpu().numpy().view(np.uint32), w.NK) if mode != "dense" else None
     return out, gmask, counts.cpu().numpy().view(np.uint32)
 
@@ -75,7 +79,7 @@ def test_causal_parity_small(dev, name, mode, beta):
         if flips:
             ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, causal_granule=g, mask=gmask)
         assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
-        frac = np.array(sb.stats(w.B, w.H)).reshape(w.B, w.H)
+        frac = np.array(sb.stats(w.B, w.H, counts=_last_counts["t"])).reshape(w.B, w.H)
         np.testing.assert_allclose(frac, gmask.sum(axis=(2, 3)) / routable_pairs(w, g), rtol=1e-6)
     else:
         assert np.all(counts == routable_pairs(w, g))
