@@ -3,6 +3,8 @@ synthetic workloads."""
 from __future__ import annotations
 
 import math
+import os
+from concurrent.futures import ProcessPoolExecutor
 
 import numpy as np
 
@@ -51,3 +53,67 @@ def small_workload(name, grid, d, bq, dtype="bf16", text_tokens=0, H=2, B=1, see
 
 def finite_beta(beta):
     return not math.isinf(beta)
+
+
+# --------------------------------------------------------------------------- whole heads, in parallel
+# The oracle evaluates a head query block by query block.  Its exponentials and key gathers
+# run on one core, so whole heads of the large workloads are evaluated as (head, block range)
+# jobs in a process pool, one BLAS thread per worker.  The arrays reach the workers through
+# fork (copy-on-write), not through pickling.
+_JOB_DATA = {}
+
+
+def _limit_blas_threads():
+    try:
+        from threadpoolctl import threadpool_limits
+        threadpool_limits(1)
+    except Exception:  # pragma: no cover - threadpoolctl is optional
+        pass
+
+
+def _oracle_job(job):
+    from oracle import sol_attn_oracle as ora
+    h, lo, hi = job
+    d = _JOB_DATA
+    mask = None if d["mask"] is None else d["mask"][h][None, None]
+    res = ora.forward(d["q"][h][None, None], d["k"][h][None, None], d["v"][h][None, None], d["block_q"],
+                      d["block_k"], d["beta"], d["mode"], keep_tail_tokens=d["keep"],
+                      query_blocks=list(range(lo, hi)), mask=mask)
+    r0, r1 = lo * d["block_q"], min(hi * d["block_q"], d["q"].shape[1])
+    return h, r0, r1, res["out"][0, 0, r0:r1]
+
+
+def pool_workers() -> int:
+    """Worker processes for oracle jobs: the CPU share of one GPU (at most 12), at least 1."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(n, 12))
+
+
+def oracle_whole_heads(q, k, v, block_q, block_k, beta, mode, mask=None, keep_tail_tokens=0, workers=None):
+    """Oracle outputs of every row of the given heads.
+
+    q, k, v: [H', N, d] float arrays (the heads to evaluate, input values as given to the GPU);
+    mask: [H', NQ, NKr] selection to use instead of routing, or None.  Returns [H', N, d] float64.
+    """
+    workers = workers or pool_workers()
+    hn, n, _ = q.shape
+    nq = -(-n // block_q)
+    per = max(1, -(-nq * hn // workers))              # one job per worker (each pools its head)
+    jobs = [(h, lo, min(lo + per, nq)) for h in range(hn) for lo in range(0, nq, per)]
+    _JOB_DATA.update(q=q, k=k, v=v, mask=mask, block_q=block_q, block_k=block_k, beta=beta, mode=mode,
+                     keep=keep_tail_tokens)
+    out = np.full(q.shape, np.nan)
+    try:
+        if workers > 1:
+            with ProcessPoolExecutor(max_workers=workers, initializer=_limit_blas_threads) as ex:
+                results = list(ex.map(_oracle_job, jobs))
+        else:
+            results = [_oracle_job(j) for j in jobs]
+    finally:
+        _JOB_DATA.clear()
+    for h, r0, r1, rows in results:
+        out[h, r0:r1] = rows
+    return out

@@ -5,7 +5,8 @@ routing): the selected fraction the library reports, the fused kernel and whole-
 times of the sparse and no-correction modes, the speedup over the library's dense mode, and
 the approximation error of both modes against exact dense attention (the fp64 oracle) on a
 sample of query blocks, together with the parity of the sparse output against the oracle run
-with the library's own mask.
+with the library's own mask once that mask has been checked against the oracle's routing
+(bit-exact outside the 1e-3 band around tau_i).
 
     python tests/sweep.py [--steps 10] [--warmup 3] [--out FILE]
     python tests/sweep.py --launch-once    # one launch per (kept, mode), for counter runs
@@ -50,6 +51,7 @@ def main():
     from oracle import sol_attn_oracle as ora
     from paper_2607_24027_amd import binding, configs, synth
     from bench import time_steps
+    from tests.parity import assert_mask_matches, errors
 
     binding.lib()
     w = configs.WORKLOADS["video720p"]
@@ -87,6 +89,8 @@ def main():
             ref = ora.forward(qs, ks, vs, w.block_q, w.block_k, 0.0, "dense", query_blocks=list(SAMPLE_BLOCKS))
             sample[h] = (qs, ks, vs, ref["out"][0, 0])
     rows = np.concatenate([np.arange(i * w.block_q, min((i + 1) * w.block_q, w.N)) for i in SAMPLE_BLOCKS])
+    # the oracle's proxies and row statistics: its routing at any cutoff is route(s_hat, mu + beta sigma)
+    routing = ora.routing(q.float().numpy(), k.float().numpy(), w.block_q, w.block_k, 0.0)
 
     results = []
     for kept in configs.SWEEP_KEPT:
@@ -99,6 +103,8 @@ def main():
         torch.cuda.synchronize()
         frac = np.array(binding.stats(w.B, w.H))
         gmask = binding.unpack_mask(mask.cpu().numpy().view(np.uint32), nkr)
+        tau = ora.thresholds(routing["mu"], routing["sigma"], beta)
+        flips = assert_mask_matches(gmask, ora.route(routing["s_hat"], tau), routing["s_hat"], tau)
         sp = time_steps(lambda: run("sparse", beta), args.steps, args.warmup)
         nc = time_steps(lambda: run("sparse_no_correction", beta), args.steps, args.warmup)
         rec = {"kept_target": kept, "beta": beta, "selected_fraction": {
@@ -107,7 +113,8 @@ def main():
                "speedup_step": round(dense["mean"] / sp["mean"], 4),
                "speedup_kernel": round(dense["kernel"] / sp["kernel"], 4),
                "speedup_no_correction_kernel": round(dense["kernel"] / nc["kernel"], 4),
-               "target_speedup": round(0.8 / max(float(frac.mean()), 1e-9), 4)}
+               "target_speedup": round(0.8 / max(float(frac.mean()), 1e-9), 4),
+               "mask_in_band_flips": flips}
         if sample:
             e_sp, e_nc, cos_sp, cos_nc, parity = [], [], [], [], []
             for h, (qs, ks, vs, ref_dense) in sample.items():
@@ -120,11 +127,12 @@ def main():
                 cos_nc.append(cosine(g_nc, rd))
                 ref_sp = ora.forward(qs, ks, vs, w.block_q, w.block_k, beta, "sparse", query_blocks=list(SAMPLE_BLOCKS),
                                      mask=gmask[0:1, h:h + 1])["out"][0, 0][rows]
-                parity.append(float(np.abs(g_sp - ref_sp).max()))
+                parity.append(errors(g_sp, ref_sp))
             rec["error_vs_dense"] = {"heads": list(SAMPLE_HEADS), "query_blocks": list(SAMPLE_BLOCKS),
                                      "rel_l2_sparse": float(np.mean(e_sp)), "rel_l2_no_correction": float(np.mean(e_nc)),
                                      "cos_sparse": float(np.mean(cos_sp)), "cos_no_correction": float(np.mean(cos_nc)),
-                                     "parity_max_abs_vs_oracle": float(np.max(parity))}
+                                     "parity_max_abs_vs_oracle": max(p[0] for p in parity),
+                                     "parity_mean_rel_vs_oracle": max(p[1] for p in parity)}
         results.append(rec)
         print(json.dumps(rec), flush=True)
     if args.out:

@@ -13,7 +13,7 @@ import torch
 from oracle import sol_attn_oracle as ora
 from paper_2607_24027_amd import binding as sb
 from paper_2607_24027_amd import configs, synth
-from tests.parity import (assert_mask_matches, assert_output_close, small_workload, to_np)
+from tests.parity import (assert_mask_matches, assert_output_close, oracle_whole_heads, small_workload, to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -292,6 +292,39 @@ def test_short_form_and_stats(dev):
     np.testing.assert_allclose(frac, (gmask.sum(axis=(2, 3)) / (w.NQ * nkr)).ravel(), rtol=1e-6)
 
 
+def test_stats_per_counts_buffer(dev):
+    # Two forwards in flight on two streams, each with its own counts buffer: sol_attn_stats
+    # returns each one's own per-head fractions (with the shape of the forward that wrote it),
+    # and refuses counts = NULL when the thread's last forward used caller-owned counts.
+    wa, (qa, ka, va) = small_inputs("bf16_d128_q128")
+    wb, (qb, kb, vb) = small_inputs("bf16_d64_q64_text")
+    ra, ma, _ = run_gpu(dev, wa, qa, ka, va, 0.8, "sparse")
+    rb, mb, _ = run_gpu(dev, wb, qb, kb, vb, 0.3, "sparse_no_correction")
+    want_a = (ma.sum(axis=(2, 3)) / (wa.NQ * wa.NK)).ravel()
+    want_b = (mb.sum(axis=(2, 3)) / (wb.NQ * (wb.NK - wb.text_tokens // 64))).ravel()
+    ca = torch.zeros((wa.B, wa.H), dtype=torch.int32, device=dev)
+    cb = torch.zeros((wb.B, wb.H), dtype=torch.int32, device=dev)
+    dev_in = [tuple(t.to(dev) for t in x) for x in ((qa, ka, va), (qb, kb, vb))]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]   # default priority
+    ws = [torch.empty(sb.workspace_bytes(w.B, w.H, w.N, w.d, w.block_q, 64, m, sb.SOL_BF16, w.text_tokens),
+                      dtype=torch.uint8, device=dev) for w, m in ((wa, "sparse"), (wb, "sparse_no_correction"))]
+    torch.cuda.synchronize()
+    with torch.cuda.stream(streams[0]):
+        sb.forward(*dev_in[0], wa.block_q, 64, 0.8, "sparse", counts=ca, workspace=ws[0])
+    with torch.cuda.stream(streams[1]):
+        sb.forward(*dev_in[1], wb.block_q, 64, 0.3, "sparse_no_correction", keep_tail_tokens=wb.text_tokens,
+                   counts=cb, workspace=ws[1])
+    np.testing.assert_allclose(sb.stats(wb.B, wb.H, counts=cb), want_b, rtol=1e-6)
+    np.testing.assert_allclose(sb.stats(wa.B, wa.H, counts=ca), want_a, rtol=1e-6)
+    with pytest.raises(sb.SolAttnError) as ei:   # the last forward on this thread wrote caller counts
+        sb.stats(wb.B, wb.H)
+    assert ei.value.code == sb.SOL_ERR_NO_DATA
+    import ctypes
+    arr = (ctypes.c_float * 2)()   # B/H other than those of the forward that wrote ca (1, 2)
+    assert sb.lib().sol_attn_stats(ctypes.cast(arr, ctypes.c_void_p), 2, 1, ca.data_ptr()) == sb.SOL_ERR_NO_DATA
+    torch.cuda.synchronize()
+
+
 def test_caller_workspace(dev):
     w, (q, k, v) = small_inputs("bf16_d64_q64_text")
     qd, kd, vd = (t.to(dev) for t in (q, k, v))
@@ -396,21 +429,30 @@ def test_full_size_sampled(dev, full, mode):
     print(f"[parity] full {w.name} mode={mode}", flush=True)
     out, gmask, counts = run_gpu(dev, w, q, k, v, beta, mode)
     heads = [(0, 0), (w.B - 1, w.H - 1)]
-    qblocks = sorted({0, 1, w.NQ // 2, w.NQ - 1})
+    # 480p and image: every query block of both heads; 720p (whose whole heads are compared at
+    # every cutoff of the kept-fraction sweep): first, second, middle and ragged last block
+    qblocks = sorted({0, 1, w.NQ // 2, w.NQ - 1}) if w.name == "video720p" else list(range(w.NQ))
     mask_for_oracle = None
     if mode != "dense":
         flips = assert_mask_matches(gmask, r["mask"], r["s_hat"], r["tau"])
         print(f"[parity] {w.name}: {flips} in-band mask flips of {gmask.size}", flush=True)
         assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
         mask_for_oracle = gmask
-    qs, ks, vs = (x[[b for b, _ in heads], [h for _, h in heads]].float().numpy()[None] for x in (q, k, v))
-    # oracle on the two sampled heads, packed as a [1, 2, N, d] problem
-    sub_mask = None if mask_for_oracle is None else mask_for_oracle[[b for b, _ in heads], [h for _, h in heads]][None]
-    ref = ora.forward(qs, ks, vs, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens,
-                      query_blocks=qblocks, mask=sub_mask)
-    got = out[[b for b, _ in heads], [h for _, h in heads]].float().cpu().numpy()[None].astype(np.float64)
+    hb, hh = [b for b, _ in heads], [h for _, h in heads]
+    qs, ks, vs = (x[hb, hh].float().numpy() for x in (q, k, v))
+    sub_mask = None if mask_for_oracle is None else mask_for_oracle[hb, hh]
+    got = out[hb, hh].float().cpu().numpy().astype(np.float64)[None]
     rows = np.concatenate([np.arange(i * w.block_q, min((i + 1) * w.block_q, w.N)) for i in qblocks])
-    assert_output_close(got[:, :, rows], ref["out"][:, :, rows], w.dtype, f"{w.name}/{mode}")
+    if len(qblocks) == w.NQ:   # whole heads: (head, block range) jobs in a process pool
+        ref_out = oracle_whole_heads(qs, ks, vs, w.block_q, 64, beta, mode, mask=sub_mask,
+                                     keep_tail_tokens=w.text_tokens)[None]
+    else:
+        ref_out = ora.forward(qs[None], ks[None], vs[None], w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens,
+                              query_blocks=qblocks, mask=None if sub_mask is None else sub_mask[None])["out"]
+    ref = {"out": ref_out}
+    max_abs, mean_rel = assert_output_close(got[:, :, rows], ref["out"][:, :, rows], w.dtype, f"{w.name}/{mode}")
+    print(f"[parity] {w.name} {mode}: {len(qblocks)} query blocks of heads {heads}, max-abs {max_abs:.3e}, "
+          f"mean-rel {mean_rel:.3e}", flush=True)
 
 
 def test_full_size_diagonal_threshold_mask(dev, full):
