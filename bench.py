@@ -112,6 +112,17 @@ def band_count(qd, kd, vd, w, beta):
     return int((s_hat - tau.double()[..., None]).abs().lt(1e-3).sum().item())
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:  # pragma: no cover
+        pass
+    return platform.processor() or platform.machine()
+
+
 def cpu_baseline(w, q, k, v, beta, seconds):
     """The fp64 oracle on the first query blocks of head (0, 0), sparse mode."""
     from oracle import sol_attn_oracle as ora
@@ -136,7 +147,56 @@ def cpu_baseline(w, q, k, v, beta, seconds):
             "seconds": round(elapsed, 3),
             "sample": f"{w.name} head (0,0), sparse mode, query blocks 0..{nblk - 1} of {w.NQ} "
                       f"({rows} of {w.N} rows), fp64 numpy; value = dense-equivalent flops of those rows / time",
-            "cpu": platform.processor() or platform.machine()}
+            "cpu": cpu_model(), "affinity_cores": len(os.sched_getaffinity(0)),
+            "threads": "cores = BLAS threads of the oracle's matrix products (its only parallel part)"}
+
+
+def measure(w, kept, qd, kd, vd, steps, warmup, modes=("sparse", "sparse_no_correction", "dense")):
+    """One workload at one calibrated cutoff: the selection of an untimed call with the debug mask
+    (kept fraction and algorithmic flops), then the timed modes.  Returns a dict of results."""
+    import torch
+    from paper_2607_24027_amd import binding, configs
+    beta = configs.beta_for(w, kept)
+    dev = qd.device
+    out = torch.empty_like(qd)
+    keep = w.text_tokens
+    n_forced = keep // w.block_k
+    nkr = w.NK - n_forced
+    mask = torch.zeros((w.B, w.H, w.NQ, binding.mask_words(nkr)), dtype=torch.int32, device=dev)
+    counts = torch.zeros((w.B, w.H), dtype=torch.int32, device=dev)
+    binding.forward(qd, kd, vd, w.block_q, w.block_k, beta, "sparse", keep, out=out, mask_out=mask, counts=counts)
+    torch.cuda.synchronize()
+    sel = binding.unpack_mask(mask.cpu().numpy().view(np.uint32), nkr)
+    stats = binding.stats(w.B, w.H, counts=counts)
+    del mask
+    exact_flop, approx_flop = algorithmic_flops(sel, w, n_forced)
+
+    def step(mode):
+        return lambda: binding.forward(qd, kd, vd, w.block_q, w.block_k, beta, mode, keep, out=out)
+
+    t = {}
+    for mode in modes:
+        log(f"timing {w.name} {mode} (kept {kept})")
+        t[mode] = time_steps(step(mode), steps, warmup)
+    return {"beta": beta, "sel": sel, "stats": stats, "exact_flop": exact_flop, "approx_flop": approx_flop,
+            "times": t}
+
+
+def summary(m, dense, w):
+    """Compact record of a measured point against a dense-mode timing of the same shape."""
+    r4 = lambda x: round(x, 4)
+    sp = m["times"]["sparse"]
+    frac = float(m["sel"].mean())
+    achieved = (m["exact_flop"] + m["approx_flop"]) / (sp["kernel"] * 1e-3) / 1e12
+    rec = {"kept": r4(frac), "beta": m["beta"],
+           "step_ms": r4(sp["mean"]), "kernel_ms": r4(sp["kernel"]),
+           "speedup_step": r4(dense["mean"] / sp["mean"]), "speedup_kernel": r4(dense["kernel"] / sp["kernel"]),
+           "target_speedup": r4(0.8 / frac),
+           "mfma_util_computed_tiles": r4(achieved / MFMA_BF16_PEAK_TFLOPS),
+           "dense_equiv_tflops": round(w.dense_flop / (sp["mean"] * 1e-3) / 1e12, 1)}
+    if "sparse_no_correction" in m["times"]:
+        rec["no_correction_kernel_ms"] = r4(m["times"]["sparse_no_correction"]["kernel"])
+    return rec
 
 
 def main():
@@ -148,6 +208,8 @@ def main():
     ap.add_argument("--kept", type=float, default=None, help="kept fraction (a calibrated sweep point)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the other sweep points and workload shapes (reported as extra keys)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="run one untimed device-to-device copy of this many MiB first (a plain copy kernel "
                          "of known size, for scaling HBM traffic counters)")
@@ -170,35 +232,17 @@ def main():
         del src, dst
     w = configs.WORKLOADS[args.workload]
     kept = w.target_kept if args.kept is None else args.kept
-    beta = configs.beta_for(w, kept)
     dev = torch.device("cuda:0")
     log(f"generating {w.name} inputs")
     q, k, v = synth.make_qkv(w, workers=synth.default_workers())
     qd, kd, vd = (x.to(dev) for x in (q, k, v))
-    out = torch.empty_like(qd)
-    keep = w.text_tokens
-    n_forced = keep // w.block_k
-    nkr = w.NK - n_forced
+    n_forced = w.text_tokens // w.block_k
 
-    # one untimed call with the debug mask for the algorithmic work and the kept fraction
-    mask = torch.zeros((w.B, w.H, w.NQ, binding.mask_words(nkr)), dtype=torch.int32, device=dev)
-    binding.forward(qd, kd, vd, w.block_q, w.block_k, beta, "sparse", keep, out=out, mask_out=mask)
-    torch.cuda.synchronize()
-    sel = binding.unpack_mask(mask.cpu().numpy().view(np.uint32), nkr)
-    del mask
+    m = measure(w, kept, qd, kd, vd, args.steps, args.warmup)
+    beta, sel, stats = m["beta"], m["sel"], m["stats"]
+    sp, nc, dn = (m["times"][x] for x in ("sparse", "sparse_no_correction", "dense"))
     frac = sel.mean(axis=(-1, -2))
-    exact_flop, approx_flop = algorithmic_flops(sel, w, n_forced)
-
-    def step(mode, b):
-        return lambda: binding.forward(qd, kd, vd, w.block_q, w.block_k, b, mode, keep, out=out)
-
-    log("timing sparse")
-    sp = time_steps(step("sparse", beta), args.steps, args.warmup)
-    stats = binding.stats(w.B, w.H)
-    log("timing sparse_no_correction")
-    nc = time_steps(step("sparse_no_correction", beta), args.steps, args.warmup)
-    log("timing dense")
-    dn = time_steps(step("dense", beta), args.steps, args.warmup)
+    exact_flop, approx_flop = m["exact_flop"], m["approx_flop"]
     band = band_count(qd, kd, vd, w, beta)
 
     sp_ms, dn_ms = sp["mean"], dn["mean"]
@@ -245,6 +289,34 @@ def main():
                      "flop_per_launch": exact_flop + approx_flop, "exact_flop": exact_flop,
                      "correction_flop": approx_flop},
     }
+    if not args.no_extras and w.name == "video720p" and args.kept is None:
+        # The other kept fractions of the 720p sweep (same inputs, same dense timing) ...
+        xs, xw = max(3, args.steps // 4), 2
+        res["sweep"] = []
+        for kp in configs.SWEEP_KEPT:
+            if kp >= 1.0:
+                continue
+            mk = measure(w, kp, qd, kd, vd, xs, xw, modes=("sparse", "sparse_no_correction"))
+            res["sweep"].append(summary(mk, dn, w))
+        # ... and the other workload shapes, each against its own dense mode
+        del qd, kd, vd
+        torch.cuda.empty_cache()
+        res["other_workloads"] = {}
+        for name in ("video480p", "image"):
+            wo = configs.WORKLOADS[name]
+            log(f"generating {wo.name} inputs")
+            qo, ko, vo = (x.to(dev) for x in synth.make_qkv(wo, workers=synth.default_workers()))
+            mo = measure(wo, wo.target_kept, qo, ko, vo, max(5, args.steps // 2), xw)
+            do = mo["times"]["dense"]
+            rec = summary(mo, do, wo)
+            rec.update({"dense_kernel_ms": round(do["kernel"], 4),
+                        "dense_mode_mfma_util": round(wo.dense_flop / (do["kernel"] * 1e-3) / 1e12
+                                                      / MFMA_BF16_PEAK_TFLOPS, 4),
+                        "shape": f"B={wo.B} H={wo.H} N={wo.N} d={wo.d} blocks {wo.block_q}x{wo.block_k}"
+                                 + (f", {wo.text_tokens} forced text tokens" if wo.text_tokens else "")})
+            res["other_workloads"][name] = rec
+            del qo, ko, vo
+            torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(w, q, k, v, beta, args.cpu_seconds)
