@@ -214,6 +214,29 @@ int sol_attn_forward_causal(const void* q, const void* k, const void* v, void* o
                             void* workspace, size_t workspace_bytes,
                             uint32_t* counts, uint32_t* mask_out, void* stream);
 
+/*
+ * Routed attention forward that allocates nothing: sol_attn_forward_ex with
+ * the library's built-in device scratch as the workspace.  For callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): it calls no hipMalloc/hipFree and
+ * no allocating library routine.
+ *
+ * Arguments as sol_attn_forward_ex without the workspace; counts is required
+ * (the library's own counts buffer would have to be allocated).  The scratch
+ * is a 64 MiB array per GPU, held from the library's load until the process
+ * ends; a shape whose sol_attn_workspace_bytes() exceeds it returns
+ * SOL_ERR_WORKSPACE before any GPU call.  Every call on one GPU uses that
+ * GPU's one array (everything it needs zeroed is cleared on the call's stream
+ * by a fill kernel), so two calls that overlap on one GPU (different streams
+ * or threads) race and give undefined results: serialise them.  The counts it
+ * writes are not tracked for sol_attn_stats (tracking creates an event):
+ * frac[b*H+h] = counts[b*H+h] / (NQ * NKr).
+ */
+int sol_attn_forward_noalloc(const void* q, const void* k, const void* v, void* out,
+                             int B, int H, int N, int d, int block_q, int block_k,
+                             float tau, int mode, int dtype, int keep_tail_tokens,
+                             uint32_t* counts, uint32_t* mask_out, void* stream);
+
 /* Device workspace bytes sol_attn_forward_ex needs for these arguments, or 0
  * if they are invalid/unsupported. */
 size_t sol_attn_workspace_bytes(int B, int H, int N, int d, int block_q, int block_k,

@@ -30,6 +30,7 @@ SIGNATURES = {
     "sol_attn_forward": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I]),
     "sol_attn_forward_ex": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _I, _I, _P, _S, _P, _P, _P]),
     "sol_attn_forward_causal": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _I, _I, _P, _S, _P, _P, _P]),
+    "sol_attn_forward_noalloc": (_I, [_P, _P, _P, _P, _I, _I, _I, _I, _I, _I, _F, _I, _I, _I, _P, _P, _P]),
     "sol_attn_workspace_bytes": (_S, [_I, _I, _I, _I, _I, _I, _I, _I, _I]),
     "sol_attn_stats": (_I, [_P, _I, _I, _P]),
     "sol_attn_timing_enable": (_I, [_I]),
@@ -251,6 +252,23 @@ def forward(q, k, v, block_q: int, block_k: int, tau: float, mode="sparse", keep
     _check(lib().sol_attn_forward_ex(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, block_q, block_k,
                                      float(tau), m, _dtype_code(q), keep_tail_tokens, ws_ptr, ws_bytes,
                                      _ptr(counts), _ptr(mask_out), _stream(q.device)))
+    return out
+
+
+def forward_noalloc(q, k, v, out, counts, block_q: int, block_k: int, tau: float, mode="sparse",
+                    keep_tail_tokens: int = 0, mask_out=None, threshold_mode: str = "exact"):
+    """sol_attn_forward_noalloc: the forward with the library's built-in scratch (no device
+    allocation by the library; out and counts are caller-owned and required)."""
+    _check_qkv(q, k, v)
+    if out is None or counts is None:
+        raise ValueError("out and counts must be given")
+    B, H, N, d = q.shape
+    nkr = -(-N // block_k) - keep_tail_tokens // block_k if block_k > 0 else 0
+    _check_forward_buffers(q, block_q, nkr, out, counts, mask_out)
+    _require_gpu(q)
+    _check(lib().sol_attn_forward_noalloc(_ptr(q), _ptr(k), _ptr(v), _ptr(out), B, H, N, d, block_q, block_k,
+                                          float(tau), _mode_code(mode, threshold_mode), _dtype_code(q),
+                                          keep_tail_tokens, _ptr(counts), _ptr(mask_out), _stream(q.device)))
     return out
 
 

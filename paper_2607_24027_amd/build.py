@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsolattn.so")
-SOURCES = ["sol_attn_kernels.hip", "sol_attn_baselines.hip", "sol_attn_api.cpp"]
+SOURCES = ["sol_attn_kernels.hip", "sol_attn_baselines.hip", "sol_attn_noalloc.hip", "sol_attn_api.cpp"]
 ARCH = os.environ.get("SOL_ATTN_ARCH", "gfx950")
 
 

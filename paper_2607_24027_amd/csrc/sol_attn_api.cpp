@@ -267,7 +267,8 @@ hipError_t note_counts(int dev, const uint32_t* counts, int B, int H, double pai
 
 int forward_impl(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d, int block_q,
                  int block_k, float tau, int mode, int dtype, int keep_tail_tokens, int causal_granule,
-                 void* workspace, size_t workspace_bytes, uint32_t* counts, uint32_t* mask_out, void* stream) {
+                 void* workspace, size_t workspace_bytes, uint32_t* counts, uint32_t* mask_out, void* stream,
+                 bool track_counts = true) {
     int rc = validate_forward(q, k, v, out, B, H, N, d, block_q, block_k, tau, mode, dtype, keep_tail_tokens,
                               causal_granule);
     if (rc) return rc;
@@ -324,10 +325,12 @@ int forward_impl(const void* q, const void* k, const void* v, void* out, int B, 
     }
     e = sol::launch_forward(s, q, k, v, out, tau, ws, counts, mask_out, st, ev0, ev1);
     if (e != hipSuccess) return hip_fail(e, "forward launch");
-    // Record where these counts came from, and when they are complete (caller holds g_mu).
-    e = note_counts(dev, counts, B, H, routable_pairs(s), counts == db.counts, st);
-    if (e != hipSuccess) return hip_fail(e, "recording the counts event");
-    t_last_counts = counts;
+    if (track_counts) {
+        // Record where these counts came from, and when they are complete (caller holds g_mu).
+        e = note_counts(dev, counts, B, H, routable_pairs(s), counts == db.counts, st);
+        if (e != hipSuccess) return hip_fail(e, "recording the counts event");
+        t_last_counts = counts;
+    }
     return ok();
 }
 
@@ -350,6 +353,26 @@ int sol_attn_forward_causal(const void* q, const void* k, const void* v, void* o
         return fail(SOL_ERR_INVALID_ARG, "causal_granule must be >= 1 (got %d)", causal_granule);
     return forward_impl(q, k, v, out, B, H, N, d, block_q, block_k, tau, mode, dtype, 0, causal_granule, workspace,
                         workspace_bytes, counts, mask_out, stream);
+}
+
+int sol_attn_forward_noalloc(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d,
+                             int block_q, int block_k, float tau, int mode, int dtype, int keep_tail_tokens,
+                             uint32_t* counts, uint32_t* mask_out, void* stream) {
+    int rc = validate_forward(q, k, v, out, B, H, N, d, block_q, block_k, tau, mode, dtype, keep_tail_tokens);
+    if (rc) return rc;
+    if (!counts) return fail(SOL_ERR_INVALID_ARG, "counts must be given: this entry point allocates nothing");
+    const sol::Shape s = sol::make_shape(B, H, N, d, block_q, block_k, mode, dtype, keep_tail_tokens);
+    const size_t need = sol::workspace_layout(s, nullptr, nullptr);
+    const size_t have = sol::noalloc_scratch_bytes();
+    if (need > have)
+        return fail(SOL_ERR_WORKSPACE,
+                    "this shape needs %zu bytes of scratch; the built-in scratch of sol_attn_forward_noalloc holds "
+                    "%zu bytes (use sol_attn_forward_ex with a workspace)", need, have);
+    void* scratch = nullptr;
+    hipError_t e = sol::noalloc_scratch(&scratch);
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    return forward_impl(q, k, v, out, B, H, N, d, block_q, block_k, tau, mode, dtype, keep_tail_tokens, 0, scratch,
+                        have, counts, mask_out, stream, /*track_counts=*/false);
 }
 
 int sol_attn_forward(const void* q, const void* k, const void* v, void* out, int B, int H, int N, int d, int block_q,

@@ -67,6 +67,12 @@ hipError_t launch_tau(const float* qbar, const float* muk, const float* cov, flo
 // Materialised-proxy routing baselines (top-k: rule 0, param = k; top-p: rule 1, param = p).
 hipError_t launch_route_materialized(const float* qbar, const float* kbar, float* shat, uint32_t* mask, int BH, int NQ,
                                      int NK, int NKr, int d, int rule, float param, hipStream_t st);
+// Built-in device scratch of the entry point that allocates nothing (one array per device in the
+// code object): its size, and its device address on the current device (looked up once per
+// device with hipGetSymbolAddress).
+size_t noalloc_scratch_bytes();
+hipError_t noalloc_scratch(void** addr);
+
 // ev_start/ev_stop (nullable) are recorded on `st` around the fused attention kernel.
 hipError_t launch_forward(const Shape& s, const void* q, const void* k, const void* v, void* out,
                           float beta, const Workspace& ws, uint32_t* counts, uint32_t* mask_out,

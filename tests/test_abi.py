@@ -23,7 +23,7 @@ def header_functions():
 def test_library_exports_every_declared_symbol():
     lib = sb.lib()
     names = header_functions()
-    assert len(names) == 12
+    assert len(names) == 13
     for name in names:
         assert hasattr(lib, name), name
     assert set(names) == set(sb.SIGNATURES)
@@ -118,6 +118,20 @@ def test_other_entry_points_validate():
     arr = (ctypes.c_float * 4)()
     assert lib.sol_attn_stats(None, 2, 2, None) == sb.SOL_ERR_INVALID_ARG
     assert lib.sol_attn_stats(ctypes.cast(arr, P), 0, 2, None) == sb.SOL_ERR_INVALID_ARG
+
+
+def test_noalloc_entry_point_validates_before_any_gpu_call():
+    lib = sb.lib()
+    na = lib.sol_attn_forward_noalloc
+    # counts are required (the library's own counts buffer would need an allocation)
+    assert na(*FAKE, 1, 2, 1000, 128, 128, 64, 0.5, 1, 0, 0, None, None, None) == sb.SOL_ERR_INVALID_ARG
+    assert "counts" in sb.last_error()
+    # a shape whose workspace exceeds the built-in scratch: a clear error, no GPU call
+    assert sb.workspace_bytes(1, 40, 75600, 128, 128, 64, "sparse") > 64 << 20
+    assert na(*FAKE, 1, 40, 75600, 128, 128, 64, 0.5, 1, 0, 0, P(0x5000), None, None) == sb.SOL_ERR_WORKSPACE
+    assert "built-in scratch" in sb.last_error()
+    # the usual validation runs first
+    assert na(*FAKE, 1, 2, 1000, 96, 128, 64, 0.5, 1, 0, 0, P(0x5000), None, None) == sb.SOL_ERR_UNSUPPORTED
 
 
 def test_stats_without_a_forward_has_no_data():
