@@ -422,10 +422,11 @@ __global__ __launch_bounds__(256) void tau_kernel(const float* __restrict__ qbar
 // Routing prologue shared by both attention kernels: the f32 proxy of every routable key
 // block (pooled query . pooled key, scaled) against the row threshold (strict >) gives its
 // selection bit for query block qi in selw (LDS); then two lists (LDS, 16-bit):
-//   list[0, NKr)   the unselected routable blocks in increasing j (sparse mode): the slots
-//                  of the correction tiles, 64 per tile, the last tile padded;
-//   list[NKr, ...) the exact tiles: selected routable blocks in increasing j, then the
-//                  forced blocks.
+//   list[0, ucap)   the unselected routable blocks in increasing j (sparse mode): the slots
+//                   of the correction tiles, 64 per tile, the last tile padded with block 0
+//                   (ucap = 64 * the chunks of routable blocks);
+//   list[ucap, ...) the exact tiles: selected routable blocks in increasing j, then the
+//                   forced blocks.
 // The online softmax is order independent, so running the correction tiles first changes
 // only the floating-point summation order.  Returns the number of exact tiles; *nuns
 // receives the number of unselected routable blocks and *nsel of selected ones.
@@ -661,7 +662,7 @@ __global__ __launch_bounds__(256) void order_kernel(const float* __restrict__ qb
 template <int D, int NT, int MODE, bool CAUSAL = false>
 __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __restrict__ kbar_h, float tau_i,
                               float beta, float scale, int NKr, int nr, int ne, int MW, float* prox, uint32_t* selw,
-                              uint16_t* list, int* scan_scratch, int* nuns, int* nsel) {
+                              uint16_t* list, int ucap, int* scan_scratch, int* nuns, int* nsel) {
     const int NC = (nr + kChunk - 1) / kChunk;   // chunks of routable blocks
     constexpr int CPR = D / 4;              // 16-byte chunks per f32 pooled-key row
     constexpr int TPK = NT / kChunk;        // threads per pooled key (1, 2 or 4)
@@ -766,8 +767,8 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
         const uint32_t hi = (2 * c + 1 < MW) ? selw[2 * c + 1] : 0u;
         return (uint64_t)lo | ((uint64_t)hi << 32);
     };
-    uint16_t* ulist = list;         // unselected routable blocks, increasing j (sparse mode)
-    uint16_t* elist = list + NKr;   // selected routable blocks, increasing j, then the forced ones
+    uint16_t* ulist = list;          // unselected routable blocks, increasing j (sparse mode), padded
+    uint16_t* elist = list + ucap;   // selected routable blocks, increasing j, then the forced ones
     // pass 1: unselected routable blocks (the correction slots)
     int n_uns = 0;
     if (MODE == kSparse) {
@@ -790,6 +791,9 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
             }
             n_uns += tot;
         }
+        // pad the last correction tile's slots with block 0 (their scores are masked), so that
+        // the tile copies read the list without bounds checks
+        for (int u = n_uns + tid; u < ((n_uns + kChunk - 1) / kChunk) * kChunk; u += NT) ulist[u] = 0;
     }
     // pass 2: selected blocks in increasing order
     int n_sel = 0;
@@ -972,9 +976,9 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
     int* scan_scratch = reinterpret_cast<int*>(rest);
     uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64);
     uint16_t* list = reinterpret_cast<uint16_t*>(rest + 64 + 4 * ((a.MW + 3) & ~3));
-    float* prox = reinterpret_cast<float*>(rest + ((64 + 4 * ((a.MW + 3) & ~3) + 2 * (a.NKr + a.NK) + 15) & ~15));
-    const uint16_t* ulist = list;            // correction slots (unselected routable blocks)
-    const uint16_t* elist = list + a.NKr;    // exact tiles
+    float* prox = reinterpret_cast<float*>(rest + ((64 + 4 * ((a.MW + 3) & ~3) + 2 * (a.NC * kChunk + a.NK) + 15) & ~15));
+    const uint16_t* ulist = list;            // correction slots (unselected routable blocks, padded)
+    const uint16_t* elist = list + a.NC * kChunk;   // exact tiles
 
     int nr = a.NKr, ne = a.NK;               // routable blocks [0, nr), forced blocks [nr, ne)
     if constexpr (CAUSAL) causal_ranges<BQ>(qi, a.causal_g, a.N, a.NK, nr, ne);
@@ -986,7 +990,8 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
         const float tau_i = CAUSAL ? 0.f : a.tau[(size_t)bh * a.NQ + qi];
         ntiles = route_and_list<D, NT, MODE, CAUSAL>(a.qbar + ((size_t)bh * a.NQ + qi) * D,
                                                      a.kbar + (size_t)bh * a.NK * D, tau_i, a.beta, a.scale, a.NKr,
-                                                     nr, ne, a.MW, prox, selw, list, scan_scratch, &nuns, &nsel);
+                                                     nr, ne, a.MW, prox, selw, list, a.NC * kChunk, scan_scratch,
+                                                     &nuns, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
@@ -1078,9 +1083,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
     // slots past the unselected blocks copy row 0, their scores are masked) into stage `buf`'s
     // K region, K layout ...
     auto slot_row = [&](int c, int r) SOL_INLINE -> int {
-        const int u = c * kChunk + r;
-        const int j = ulist[min(u, nuns - 1)];   // nuns >= 1 whenever a correction tile exists
-        return u < nuns ? j : 0;
+        return ulist[c * kChunk + r];   // padding slots of the last tile hold block 0
     };
     const char* kbh_base = reinterpret_cast<const char*>(a.kbarh + (size_t)bh * a.NC * kChunk * D);
     const char* vbh_base = reinterpret_cast<const char*>(a.vbarh + (size_t)bh * a.NC * kChunk * D);
@@ -1752,9 +1755,9 @@ __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
     int* scan_scratch = reinterpret_cast<int*>(rest);
     uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64);
     uint16_t* list = reinterpret_cast<uint16_t*>(rest + 64 + 4 * ((a.MW + 3) & ~3));
-    float* prox = reinterpret_cast<float*>(rest + ((64 + 4 * ((a.MW + 3) & ~3) + 2 * (a.NKr + a.NK) + 15) & ~15));
-    const uint16_t* ulist = list;            // correction slots (unselected routable blocks)
-    const uint16_t* elist = list + a.NKr;    // exact tiles
+    float* prox = reinterpret_cast<float*>(rest + ((64 + 4 * ((a.MW + 3) & ~3) + 2 * (a.NC * kChunk + a.NK) + 15) & ~15));
+    const uint16_t* ulist = list;            // correction slots (unselected routable blocks, padded)
+    const uint16_t* elist = list + a.NC * kChunk;   // exact tiles
 
     const int bh = blockIdx.y, qi = blockIdx.x, tid = threadIdx.x;
     int nr = a.NKr, ne = a.NK;               // routable blocks [0, nr), forced blocks [nr, ne)
@@ -1767,7 +1770,8 @@ __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
         const float tau_i = CAUSAL ? 0.f : a.tau[(size_t)bh * a.NQ + qi];
         ntiles = route_and_list<D, NT, MODE, CAUSAL>(a.qbar + ((size_t)bh * a.NQ + qi) * D,
                                                      a.kbar + (size_t)bh * a.NK * D, tau_i, a.beta, a.scale, a.NKr,
-                                                     nr, ne, a.MW, prox, selw, list, scan_scratch, &nuns, &nsel);
+                                                     nr, ne, a.MW, prox, selw, list, a.NC * kChunk, scan_scratch,
+                                                     &nuns, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
@@ -1948,7 +1952,7 @@ Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype
 }
 
 size_t attn_lds_bytes(const Shape& s) {
-    size_t rest = 64 + 4 * (size_t)((s.MW + 3) & ~3) + 2 * (size_t)(s.NKr + s.NK);
+    size_t rest = 64 + 4 * (size_t)((s.MW + 3) & ~3) + 2 * ((size_t)s.NC * kChunk + s.NK);
     if (s.causal && s.mode != kDense) rest = ((rest + 15) & ~(size_t)15) + 4 * (size_t)s.NKr;   // proxies of a row
     if (s.dtype == kBF16) {
         const size_t stage = (size_t)kBlockK * s.d * 2 * 2;
