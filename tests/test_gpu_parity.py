@@ -273,6 +273,42 @@ def test_beta_minus_inf_is_bitwise_dense(dev, name):
         assert torch.equal(out, dense)
 
 
+@pytest.mark.parametrize("name", ["bf16_d128_q128", "bf16_d64_q64_text"])
+@pytest.mark.parametrize("qf,kf,modes", [(2e-5, 5e4, ("sparse_no_correction",)),
+                                         (1.0, 1e-6, ("sparse", "sparse_no_correction"))],
+                         ids=["large_keys", "subnormal_keys"])
+def test_routing_outside_the_f16_normal_range(dev, name, qf, kf, modes):
+    # Routing takes f32 proxies from the f32 pooled means, while the pre-pass also writes f16
+    # copies of the pooled keys (read by the correction tiles only).  Inputs at both ends of the
+    # f16 range must leave the selection and the no-correction outputs unaffected:
+    # * keys x5e4, queries x2e-5: the logits keep their scale, most pooled-key rows have a
+    #   component past the f16 range (65504) and the pooled queries are f16 subnormals (the range
+    #   contract on k applies to SOL_SPARSE only, so only the no-correction mode runs);
+    # * keys x1e-6: the pooled keys are f16 subnormals, and the proxies scale by 1e-6.
+    # The mask must match the oracle's routing, with the band scaled as the proxies are, and the
+    # outputs the oracle's.
+    w, (q, k, v) = small_inputs(name)
+    q = (q.float() * qf).to(q.dtype)
+    k = (k.float() * kf).to(k.dtype)
+    kbar = np.abs(ora.pool_means(to_np(k), 64)[0])
+    if kf > 1:
+        assert (kbar > 65504).any(axis=-1).mean() > 0.3
+    else:
+        assert np.median(kbar) < 2.0 ** -14   # below the smallest normal f16
+    qn, kn, vn = to_np(q), to_np(k), to_np(v)
+    for mode in modes:
+        for beta in (0.8, -0.3):
+            print(f"[parity] {name} q x{qf} k x{kf} {mode} beta={beta}", flush=True)
+            out, gmask, counts = run_gpu(dev, w, q, k, v, beta, mode)
+            ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens)
+            flips = assert_mask_matches(gmask, ref["mask"], ref["s_hat"], ref["tau"], band=1e-3 * qf * kf)
+            if flips:
+                ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens,
+                                  mask=gmask)
+            assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
+            assert_output_close(to_np(out), ref["out"], w.dtype, f"{name}/q x{qf} k x{kf}/{mode}/{beta}")
+
+
 def test_no_correction_with_nothing_selected_is_zero(dev):
     w, (q, k, v) = small_inputs("bf16_d128_q128")
     out, gmask, counts = run_gpu(dev, w, q, k, v, INF, "sparse_no_correction")
