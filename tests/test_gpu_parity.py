@@ -46,7 +46,7 @@ def small_inputs(name):
     return _cache[name]
 
 
-def run_gpu(dev, w, q, k, v, beta, mode, want_mask=True, threshold_mode="exact"):
+def run_gpu(dev, w, q, k, v, beta, mode, want_mask=True, threshold_mode="exact", outputs_defined=True):
     qd, kd, vd = (t.to(dev) for t in (q, k, v))
     nkr = w.NK - w.text_tokens // 64
     mw = sb.mask_words(nkr)
@@ -58,7 +58,8 @@ def run_gpu(dev, w, q, k, v, beta, mode, want_mask=True, threshold_mode="exact")
     sb.forward(qd, kd, vd, w.block_q, 64, beta, mode, keep_tail_tokens=w.text_tokens, out=out,
                counts=counts, mask_out=mask, threshold_mode=threshold_mode)
     torch.cuda.synchronize()
-    assert bool(torch.isfinite(out).all()), f"{w.name}/{mode}: rows left unwritten"
+    if outputs_defined:
+        assert bool(torch.isfinite(out).all()), f"{w.name}/{mode}: rows left unwritten"
     gmask = None
     if want_mask and mode != "dense":
         gmask = sb.unpack_mask(mask.cpu().numpy().view(np.uint32), nkr)
@@ -307,6 +308,14 @@ def test_routing_outside_the_f16_normal_range(dev, name, qf, kf, modes):
                                   mask=gmask)
             assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
             assert_output_close(to_np(out), ref["out"], w.dtype, f"{name}/q x{qf} k x{kf}/{mode}/{beta}")
+    if kf > 1:
+        # SOL_SPARSE with pooled keys past the f16 range is outside its contract: the correction
+        # tiles' f16 pooled keys overflow, so its outputs are not defined.  What stays defined is
+        # what the f32 routing produces: the mask and the counts.
+        out, gmask, counts = run_gpu(dev, w, q, k, v, 0.8, "sparse", outputs_defined=False)
+        ref = ora.routing(qn, kn, w.block_q, 64, 0.8, keep_tail_tokens=w.text_tokens)
+        assert_mask_matches(gmask, ref["mask"], ref["s_hat"], ref["tau"], band=1e-3 * qf * kf)
+        assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
 
 
 def test_no_correction_with_nothing_selected_is_zero(dev):
