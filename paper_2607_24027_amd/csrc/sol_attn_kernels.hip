@@ -662,7 +662,7 @@ __global__ __launch_bounds__(256) void order_kernel(const float* __restrict__ qb
 template <int D, int NT, int MODE, bool CAUSAL = false>
 __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __restrict__ kbar_h, float tau_i,
                               float beta, float scale, int NKr, int nr, int ne, int MW, float* prox, uint32_t* selw,
-                              uint16_t* list, int ucap, int* scan_scratch, int* nuns, int* nsel) {
+                              uint16_t* list, int ucap, int* scan_scratch, int* wpre, int* nuns, int* nsel) {
     const int NC = (nr + kChunk - 1) / kChunk;   // chunks of routable blocks
     constexpr int CPR = D / 4;              // 16-byte chunks per f32 pooled-key row
     constexpr int TPK = NT / kChunk;        // threads per pooled key (1, 2 or 4)
@@ -762,55 +762,34 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
         }
         __syncthreads();
     }
-    auto chunk_bits = [&](int c) -> uint64_t {
-        const uint32_t lo = selw[2 * c];
-        const uint32_t hi = (2 * c + 1 < MW) ? selw[2 * c + 1] : 0u;
-        return (uint64_t)lo | ((uint64_t)hi << 32);
-    };
     uint16_t* ulist = list;          // unselected routable blocks, increasing j (sparse mode), padded
     uint16_t* elist = list + ucap;   // selected routable blocks, increasing j, then the forced ones
-    // pass 1: unselected routable blocks (the correction slots)
-    int n_uns = 0;
-    if (MODE == kSparse) {
-        for (int c0 = 0; c0 < NC; c0 += NT) {
-            const int c = c0 + tid;
-            uint64_t ub = 0;
-            if (c < NC) {
-                const int nvalid = min(kChunk, nr - c * kChunk);
-                const uint64_t valid = nvalid >= 64 ? ~0ull : ((1ull << nvalid) - 1ull);
-                ub = ~chunk_bits(c) & valid;
-            }
-            const int nu = __popcll(ub);
-            int tot;
-            const int incl = block_scan_incl<NT>(nu, scan_scratch, &tot);
-            int pos = n_uns + incl - nu;
-            while (ub) {
-                const int b = __builtin_ctzll(ub);
-                ub &= ub - 1;
-                ulist[pos++] = (uint16_t)(c * kChunk + b);
-            }
-            n_uns += tot;
-        }
-        // pad the last correction tile's slots with block 0 (their scores are masked), so that
-        // the tile copies read the list without bounds checks
-        for (int u = n_uns + tid; u < ((n_uns + kChunk - 1) / kChunk) * kChunk; u += NT) ulist[u] = 0;
-    }
-    // pass 2: selected blocks in increasing order
+    // Both lists in one pass with a thread per block: a scan of the words' popcounts gives the
+    // selected blocks before each word, a popcount within the word those before block j; j is
+    // then selected block number `before` and, if not selected, unselected block j - before.
+    const int MWr = (nr + 31) >> 5;  // words holding routable bits (bits past nr are zero)
     int n_sel = 0;
-    for (int c0 = 0; c0 < NC; c0 += NT) {
-        const int c = c0 + tid;
-        uint64_t bits = c < NC ? chunk_bits(c) : 0ull;
-        const int ns = __popcll(bits);
+    for (int w0 = 0; w0 < MWr; w0 += NT) {
+        const int w = w0 + tid;
+        const int cnt = w < MWr ? __popc(selw[w]) : 0;
         int tot;
-        const int incl = block_scan_incl<NT>(ns, scan_scratch, &tot);
-        int pos = n_sel + incl - ns;
-        while (bits) {
-            const int b = __builtin_ctzll(bits);
-            bits &= bits - 1;
-            elist[pos++] = (uint16_t)(c * kChunk + b);
-        }
+        const int incl = block_scan_incl<NT>(cnt, scan_scratch, &tot);
+        if (w < MWr) wpre[w] = n_sel + incl - cnt;
         n_sel += tot;
     }
+    __syncthreads();
+    for (int j = tid; j < nr; j += NT) {
+        const uint32_t word = selw[j >> 5];
+        const int b = j & 31;
+        const int before = wpre[j >> 5] + __popc(word & ((1u << b) - 1u));
+        if ((word >> b) & 1u) elist[before] = (uint16_t)j;
+        else if (MODE == kSparse) ulist[j - before] = (uint16_t)j;
+    }
+    const int n_uns = MODE == kSparse ? nr - n_sel : 0;
+    // pad the last correction tile's slots with block 0 (their scores are masked), so that the
+    // tile copies read the list without bounds checks
+    if (MODE == kSparse)
+        for (int u = n_uns + tid; u < ((n_uns + kChunk - 1) / kChunk) * kChunk; u += NT) ulist[u] = 0;
     for (int j = nr + tid; j < ne; j += NT) elist[n_sel + (j - nr)] = (uint16_t)j;
     __syncthreads();
     *nuns = n_uns;
@@ -976,7 +955,8 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
     int* scan_scratch = reinterpret_cast<int*>(rest);
     uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64);
     uint16_t* list = reinterpret_cast<uint16_t*>(rest + 64 + 4 * ((a.MW + 3) & ~3));
-    float* prox = reinterpret_cast<float*>(rest + ((64 + 4 * ((a.MW + 3) & ~3) + 2 * (a.NC * kChunk + a.NK) + 15) & ~15));
+    int* wpre = reinterpret_cast<int*>(rest + ((64 + 4 * ((a.MW + 3) & ~3) + 2 * (a.NC * kChunk + a.NK) + 15) & ~15));
+    float* prox = reinterpret_cast<float*>(wpre + ((a.MW + 3) & ~3));   // after the word prefixes
     const uint16_t* ulist = list;            // correction slots (unselected routable blocks, padded)
     const uint16_t* elist = list + a.NC * kChunk;   // exact tiles
 
@@ -991,7 +971,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
         ntiles = route_and_list<D, NT, MODE, CAUSAL>(a.qbar + ((size_t)bh * a.NQ + qi) * D,
                                                      a.kbar + (size_t)bh * a.NK * D, tau_i, a.beta, a.scale, a.NKr,
                                                      nr, ne, a.MW, prox, selw, list, a.NC * kChunk, scan_scratch,
-                                                     &nuns, &nsel);
+                                                     wpre, &nuns, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
@@ -1755,7 +1735,8 @@ __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
     int* scan_scratch = reinterpret_cast<int*>(rest);
     uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64);
     uint16_t* list = reinterpret_cast<uint16_t*>(rest + 64 + 4 * ((a.MW + 3) & ~3));
-    float* prox = reinterpret_cast<float*>(rest + ((64 + 4 * ((a.MW + 3) & ~3) + 2 * (a.NC * kChunk + a.NK) + 15) & ~15));
+    int* wpre = reinterpret_cast<int*>(rest + ((64 + 4 * ((a.MW + 3) & ~3) + 2 * (a.NC * kChunk + a.NK) + 15) & ~15));
+    float* prox = reinterpret_cast<float*>(wpre + ((a.MW + 3) & ~3));   // after the word prefixes
     const uint16_t* ulist = list;            // correction slots (unselected routable blocks, padded)
     const uint16_t* elist = list + a.NC * kChunk;   // exact tiles
 
@@ -1771,7 +1752,7 @@ __global__ __launch_bounds__(BQ) void routed_attn_f32_kernel(AttnArgsF32 a) {
         ntiles = route_and_list<D, NT, MODE, CAUSAL>(a.qbar + ((size_t)bh * a.NQ + qi) * D,
                                                      a.kbar + (size_t)bh * a.NK * D, tau_i, a.beta, a.scale, a.NKr,
                                                      nr, ne, a.MW, prox, selw, list, a.NC * kChunk, scan_scratch,
-                                                     &nuns, &nsel);
+                                                     wpre, &nuns, &nsel);
         if (a.mask_out)
             for (int w = tid; w < a.MW; w += NT) a.mask_out[((size_t)bh * a.NQ + qi) * a.MW + w] = selw[w];
     }
@@ -1952,8 +1933,10 @@ Shape make_shape(int B, int H, int N, int d, int bq, int bk, int mode, int dtype
 }
 
 size_t attn_lds_bytes(const Shape& s) {
+    // scan scratch, selection words, lists, then (16-byte aligned) the words' prefix counts
     size_t rest = 64 + 4 * (size_t)((s.MW + 3) & ~3) + 2 * ((size_t)s.NC * kChunk + s.NK);
-    if (s.causal && s.mode != kDense) rest = ((rest + 15) & ~(size_t)15) + 4 * (size_t)s.NKr;   // proxies of a row
+    rest = ((rest + 15) & ~(size_t)15) + 4 * (size_t)((s.MW + 3) & ~3);
+    if (s.causal && s.mode != kDense) rest += 4 * (size_t)s.NKr;   // proxies of a row
     if (s.dtype == kBF16) {
         const size_t stage = (size_t)kBlockK * s.d * 2 * 2;
         return 2 * stage + rest;
