@@ -694,8 +694,12 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
             a3 = fmaf(qv[i][3], kv[i][3], a3);
         }
         float dot = (a0 + a1) + (a2 + a3);
-#pragma unroll
-        for (int off = 1; off < TPK; off <<= 1) dot += __shfl_xor(dot, off);
+        // the TPK lanes of a key are consecutive lanes of one quad: reduce with quad
+        // permutations (DPP), which stay in the VALU instead of going through the LDS crossbar
+        if constexpr (TPK >= 2)
+            dot += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(dot), 0xB1, 0xF, 0xF, false));
+        if constexpr (TPK >= 4)
+            dot += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(dot), 0x4E, 0xF, 0xF, false));
         const int j = c * kChunk + jl;
         if constexpr (CAUSAL) {
             if (seg == 0 && j < nr) prox[j] = scale * dot;
@@ -703,9 +707,22 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
         }
         const bool sel = j < nr && scale * dot > tau_i;
         const uint64_t bal = __ballot(sel);
-        uint64_t bits = 0;
-#pragma unroll
-        for (int t = 0; t < KPWV; ++t) bits |= ((bal >> (TPK * t)) & 1ull) << t;
+        // every TPK-th ballot bit (all lanes of a key agree): compress them into KPWV bits
+        uint64_t bits = bal;
+        if constexpr (TPK == 4) {
+            bits &= 0x1111111111111111ull;
+            bits = (bits | (bits >> 3)) & 0x0303030303030303ull;
+            bits = (bits | (bits >> 6)) & 0x000F000F000F000Full;
+            bits = (bits | (bits >> 12)) & 0x000000FF000000FFull;
+            bits = (bits | (bits >> 24)) & 0xFFFFull;
+        } else if constexpr (TPK == 2) {
+            bits &= 0x5555555555555555ull;
+            bits = (bits | (bits >> 1)) & 0x3333333333333333ull;
+            bits = (bits | (bits >> 2)) & 0x0F0F0F0F0F0F0F0Full;
+            bits = (bits | (bits >> 4)) & 0x00FF00FF00FF00FFull;
+            bits = (bits | (bits >> 8)) & 0x0000FFFF0000FFFFull;
+            bits = (bits | (bits >> 16)) & 0xFFFFFFFFull;
+        }
         if (lane == 0) {
             const int bit0 = c * kChunk + wave * KPWV;
             if constexpr (KPWV == 64) {
@@ -721,18 +738,28 @@ __device__ int route_and_list(const float* __restrict__ qbar_i, const float* __r
     // ring of NB groups in flight (fewer when a thread's share of a row is large)
     constexpr int NB = CPT <= 8 ? 3 : (CPT <= 16 ? 2 : 1);
     f32x4 kb[NB][CPT];
+    // Loads of rows past the routable keys are clamped to the last one, so they are always
+    // issued: with no conditional load in the steady-state loop the compiler's wait counts
+    // cover exactly the group being decided and the other NB - 1 groups stay in flight.
 #pragma unroll
-    for (int b = 0; b < NB; ++b)
-        if (b < NC) load(b, kb[b]);
-    for (int c = 0; c < NC; c += NB) {
+    for (int b = 0; b < NB; ++b) load(b, kb[b]);
+    int c = 0;
+    for (; c + 2 * NB <= NC; c += NB) {
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
-            if (c + b < NC) {
-                decide(c + b, kb[b]);
-                if (c + b + NB < NC) load(c + b + NB, kb[b]);
-            }
+            decide(c + b, kb[b]);
+            load(c + b + NB, kb[b]);
         }
     }
+    // tail: fewer than 2 NB groups left (all of them when NC < NB)
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        if (c + b < NC) decide(c + b, kb[b]);
+        if (c + b + NB < NC) load(c + b + NB, kb[b]);
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+        if (c + NB + b < NC) decide(c + NB + b, kb[b]);
     __syncthreads();
     if constexpr (CAUSAL) {
         // row statistics over the routable prefix, then the selection bits of every word
