@@ -247,13 +247,16 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict
 
 // ---------------------------------------------------------------------------
 // Moments of the routable pooled keys (Eq. threshold_stats_exact, centred form), in two
-// kernels.  moments_partial_kernel: grid (kMomSplit, BH), 256 threads; split s accumulates,
+// kernels.  moments_partial_kernel: grid (mom_splits(BH), BH), 256 threads; split s accumulates,
 // in f64, S1 = sum_j x_j and S2 = sum_j x_j^T x_j over its share of the key blocks, with
 // x_j = Kbar_j - Kbar_0 (a shift that keeps the second moment well conditioned).
 // moments_final_kernel: grid (D*D/256, BH), sums the splits and writes mu_K = Kbar_0 + S1/n
 // and C_K = S2/n - (S1/n)^T (S1/n) in f32, 256 entries of C_K per workgroup.
 // ---------------------------------------------------------------------------
-constexpr int kMomSplit = 16;
+// Splits per head: as many as fill one round of the device's resident workgroups (two per CU
+// at this kernel's register use), at most 32.
+constexpr int kMomMaxSplit = 32;
+int mom_splits(int BH) { return std::max(1, std::min(kMomMaxSplit, 512 / std::max(BH, 1))); }
 
 // Device lambdas of the attention kernel are always inlined: a call would move the register
 // tile state through memory.
@@ -261,7 +264,7 @@ constexpr int kMomSplit = 16;
 
 template <int D>
 __device__ __forceinline__ void moments_partial_block(const float* __restrict__ kbar, double* __restrict__ part, int NK,
-                                                      int NKr, int sp, int bh) {
+                                                      int NKr, int sp, int bh, int nsplit) {
     constexpr int SLAB = 32;
     constexpr int TS = D + 4;                  // f32 row stride of the staged slab
     constexpr int RB = D / 16;                 // 16x16 thread grid, RB x RB entries each
@@ -269,7 +272,7 @@ __device__ __forceinline__ void moments_partial_block(const float* __restrict__ 
     __shared__ float k0[D];
     const int t = threadIdx.x;
     const float* kb = kbar + (size_t)bh * NK * D;
-    const int j0 = (int)((long long)NKr * sp / kMomSplit), j1 = (int)((long long)NKr * (sp + 1) / kMomSplit);
+    const int j0 = (int)((long long)NKr * sp / nsplit), j1 = (int)((long long)NKr * (sp + 1) / nsplit);
     for (int c = t; c < D; c += 256) k0[c] = kb[c];
     __syncthreads();
     const int r0 = (t / 16) * RB, c0 = (t % 16) * RB;
@@ -298,7 +301,7 @@ __device__ __forceinline__ void moments_partial_block(const float* __restrict__ 
         }
         __syncthreads();
     }
-    double* out = part + ((size_t)bh * kMomSplit + sp) * (D * D + D);
+    double* out = part + ((size_t)bh * nsplit + sp) * (D * D + D);
 #pragma unroll
     for (int u = 0; u < RB; ++u)
 #pragma unroll
@@ -308,22 +311,22 @@ __device__ __forceinline__ void moments_partial_block(const float* __restrict__ 
 
 template <int D>
 __global__ __launch_bounds__(256) void moments_partial_kernel(const float* __restrict__ kbar, double* __restrict__ part,
-                                                              int NK, int NKr) {
-    moments_partial_block<D>(kbar, part, NK, NKr, blockIdx.x, blockIdx.y);
+                                                              int NK, int NKr, int nsplit) {
+    moments_partial_block<D>(kbar, part, NK, NKr, blockIdx.x, blockIdx.y, nsplit);
 }
 
 
 template <int D>
 __global__ __launch_bounds__(256) void moments_final_kernel(const float* __restrict__ kbar, const double* __restrict__ part,
                                                             float* __restrict__ muk, float* __restrict__ cov, int NK,
-                                                            int NKr) {
+                                                            int NKr, int nsplit) {
     __shared__ double m[D];
     const int chunk = blockIdx.x, bh = blockIdx.y, t = threadIdx.x;
-    const double* pp = part + (size_t)bh * kMomSplit * (D * D + D);
+    const double* pp = part + (size_t)bh * nsplit * (D * D + D);
     const double inv = 1.0 / (double)NKr;
     for (int c = t; c < D; c += 256) {
         double s = 0.0;
-        for (int sp = 0; sp < kMomSplit; ++sp) s += pp[(size_t)sp * (D * D + D) + D * D + c];
+        for (int sp = 0; sp < nsplit; ++sp) s += pp[(size_t)sp * (D * D + D) + D * D + c];
         m[c] = s * inv;
         if (chunk == 0) muk[(size_t)bh * D + c] = (float)((double)kbar[(size_t)bh * NK * D + c] + m[c]);
     }
@@ -331,7 +334,7 @@ __global__ __launch_bounds__(256) void moments_final_kernel(const float* __restr
     const int e = chunk * 256 + t;
     if (e < D * D) {
         double s = 0.0;
-        for (int sp = 0; sp < kMomSplit; ++sp) s += pp[(size_t)sp * (D * D + D) + e];
+        for (int sp = 0; sp < nsplit; ++sp) s += pp[(size_t)sp * (D * D + D) + e];
         cov[(size_t)bh * D * D + e] = (float)(s * inv - m[e / D] * m[e % D]);
     }
 }
@@ -532,7 +535,9 @@ __device__ float2 block_sum2(float x, float y, float2* scratch) {
     return tot;
 }
 
-template <int D>
+// KPT: query blocks ranked per thread, a power of two with 256 * KPT >= NQ (the launch picks the
+// smallest), so that the rank loop runs no empty slots.
+template <int D, int KPT>
 __global__ __launch_bounds__(256) void order_kernel(const float* __restrict__ qbar, const float* __restrict__ cov,
                                                     const float* __restrict__ sigma, uint16_t* __restrict__ order,
                                                     int NQ) {
@@ -547,7 +552,7 @@ __global__ __launch_bounds__(256) void order_kernel(const float* __restrict__ qb
     __shared__ __attribute__((aligned(16))) uint32_t keys[kOrderMaxNQ];
     const int bh = blockIdx.x, t = threadIdx.x, lane = t & 63, wave = t >> 6;
     uint16_t* ord = order + (size_t)bh * NQ;
-    if (NQ > kOrderMaxNQ) {
+    if (NQ > kOrderMaxNQ || NQ > NT * KPT) {
         for (int i = t; i < NQ; i += NT) ord[i] = (uint16_t)i;
         return;
     }
@@ -634,7 +639,7 @@ __global__ __launch_bounds__(256) void order_kernel(const float* __restrict__ qb
     __syncthreads();
     // rank sort: block i goes to position |{j : key_j < key_i}|.  Each thread ranks all of its
     // keys (at most KPT) in one pass over the keys, read four at a time.
-    constexpr int KPT = kOrderMaxNQ / NT;
+    static_assert(NT * KPT <= kOrderMaxNQ, "rank slots exceed the key buffer");
     uint32_t mine[KPT];
     int rank[KPT];
 #pragma unroll
@@ -2015,21 +2020,24 @@ hipError_t launch_pool_mean(const void* x, float* mean, int dtype, int BH, int N
     return hipGetLastError();
 }
 
-size_t moments_scratch_bytes(int BH, int d) { return (size_t)BH * kMomSplit * ((size_t)d * d + d) * sizeof(double); }
+size_t moments_scratch_bytes(int BH, int d) { return (size_t)BH * mom_splits(BH) * ((size_t)d * d + d) * sizeof(double); }
 
 hipError_t launch_moments_final(const float* kbar, float* muk, float* cov, double* scratch, int BH, int NK, int NKr,
                                 int d, hipStream_t st) {
     if (d == 128)
-        moments_final_kernel<128><<<dim3(128 * 128 / 256, BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr);
+        moments_final_kernel<128><<<dim3(128 * 128 / 256, BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr,
+                                                                                    mom_splits(BH));
     else
-        moments_final_kernel<64><<<dim3(64 * 64 / 256, BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr);
+        moments_final_kernel<64><<<dim3(64 * 64 / 256, BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr,
+                                                                                  mom_splits(BH));
     return hipGetLastError();
 }
 
 hipError_t launch_moments(const float* kbar, float* muk, float* cov, double* scratch, int BH, int NK, int NKr, int d,
                           hipStream_t st) {
-    if (d == 128) moments_partial_kernel<128><<<dim3(kMomSplit, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr);
-    else moments_partial_kernel<64><<<dim3(kMomSplit, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr);
+    const int ns = mom_splits(BH);
+    if (d == 128) moments_partial_kernel<128><<<dim3(ns, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr, ns);
+    else moments_partial_kernel<64><<<dim3(ns, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr, ns);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_moments_final(kbar, muk, cov, scratch, BH, NK, NKr, d, st);
@@ -2056,6 +2064,24 @@ hipError_t launch_tau(const float* qbar, const float* muk, const float* cov, flo
 // V^T, 4*Npad*d bytes per head) within kMallBudget of the shared MALL.  Heads differ in their
 // kept fraction, so the XCDs of one head may finish early; the queues' stealing evens that out.
 constexpr double kMallBudget = 96.0 * 1024 * 1024;
+template <int D>
+hipError_t launch_order_d(const float* qbar, const float* cov, const float* sigma, uint16_t* order, int BH, int NQ,
+                          hipStream_t st) {
+    const dim3 grid(BH), block(256);
+    if (NQ <= 256) order_kernel<D, 1><<<grid, block, 0, st>>>(qbar, cov, sigma, order, NQ);
+    else if (NQ <= 512) order_kernel<D, 2><<<grid, block, 0, st>>>(qbar, cov, sigma, order, NQ);
+    else if (NQ <= 1024) order_kernel<D, 4><<<grid, block, 0, st>>>(qbar, cov, sigma, order, NQ);
+    else if (NQ <= 2048) order_kernel<D, 8><<<grid, block, 0, st>>>(qbar, cov, sigma, order, NQ);
+    else order_kernel<D, 16><<<grid, block, 0, st>>>(qbar, cov, sigma, order, NQ);
+    return hipGetLastError();
+}
+
+hipError_t launch_order(const float* qbar, const float* cov, const float* sigma, uint16_t* order, int BH, int NQ, int d,
+                        hipStream_t st) {
+    return d == 128 ? launch_order_d<128>(qbar, cov, sigma, order, BH, NQ, st)
+                    : launch_order_d<64>(qbar, cov, sigma, order, BH, NQ, st);
+}
+
 int heads_in_flight_log2(const Shape& s) {
     const double kv = 4.0 * (double)s.Npad * s.d;
     int hl = 0;
@@ -2089,9 +2115,7 @@ hipError_t launch_forward(const Shape& s, const void* q, const void* k, const vo
                 if ((e = launch_tau(ws.qbar, ws.muk, ws.cov, ws.tau, nullptr, ws.sigma, s.BH, s.NQ, d, beta, s.diag,
                                     st)) != hipSuccess)
                     return e;
-                if (d == 128) order_kernel<128><<<dim3(s.BH), dim3(256), 0, st>>>(ws.qbar, ws.cov, ws.sigma, ws.order, s.NQ);
-                else order_kernel<64><<<dim3(s.BH), dim3(256), 0, st>>>(ws.qbar, ws.cov, ws.sigma, ws.order, s.NQ);
-                if ((e = hipGetLastError()) != hipSuccess) return e;
+                if ((e = launch_order(ws.qbar, ws.cov, ws.sigma, ws.order, s.BH, s.NQ, d, st)) != hipSuccess) return e;
             }
         }
         AttnArgs a{};
