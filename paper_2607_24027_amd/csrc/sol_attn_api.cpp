@@ -155,7 +155,7 @@ int sol_attn_thresholds(const float* qbar, const float* kbar, float* tau, float*
     const int BH = B * H;
     // Moment buffers are temporary: allocate, run, wait, free (this entry point synchronises).
     void* mom = nullptr;
-    const size_t part = sol::moments_scratch_bytes(BH, d);
+    const size_t part = sol::moments_scratch_bytes(BH, nk_routable, d);
     hipError_t e = hipMalloc(&mom, part + ((size_t)BH * d * d + (size_t)BH * d) * sizeof(float));
     if (e != hipSuccess) return hip_fail(e, "hipMalloc(moments)");
     double* scratch = static_cast<double*>(mom);

@@ -57,7 +57,7 @@ size_t attn_lds_bytes(const Shape& s);
 
 hipError_t launch_pool_mean(const void* x, float* mean, int dtype, int BH, int N, int d, int blk,
                             hipStream_t st);
-size_t moments_scratch_bytes(int BH, int d);
+size_t moments_scratch_bytes(int BH, int NKr, int d);
 hipError_t launch_moments_final(const float* kbar, float* muk, float* cov, double* scratch, int BH, int NK, int NKr,
                                 int d, hipStream_t st);
 hipError_t launch_moments(const float* kbar, float* muk, float* cov, double* scratch, int BH, int NK, int NKr,

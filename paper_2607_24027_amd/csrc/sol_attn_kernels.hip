@@ -247,16 +247,19 @@ __global__ __launch_bounds__(256) void prep_kv_kernel(const uint16_t* __restrict
 
 // ---------------------------------------------------------------------------
 // Moments of the routable pooled keys (Eq. threshold_stats_exact, centred form), in two
-// kernels.  moments_partial_kernel: grid (mom_splits(BH), BH), 256 threads; split s accumulates,
+// kernels.  moments_partial_kernel: grid (mom_splits(BH, NKr), BH), 256 threads; split s accumulates,
 // in f64, S1 = sum_j x_j and S2 = sum_j x_j^T x_j over its share of the key blocks, with
 // x_j = Kbar_j - Kbar_0 (a shift that keeps the second moment well conditioned).
 // moments_final_kernel: grid (D*D/256, BH), sums the splits and writes mu_K = Kbar_0 + S1/n
 // and C_K = S2/n - (S1/n)^T (S1/n) in f32, 256 entries of C_K per workgroup.
 // ---------------------------------------------------------------------------
 // Splits per head: as many as fill one round of the device's resident workgroups (two per CU
-// at this kernel's register use), at most 32.
+// at this kernel's register use), at most 32, and at least 32 pooled keys each (a split
+// writes a d x d f64 partial, which the final kernel reads back).
 constexpr int kMomMaxSplit = 32;
-int mom_splits(int BH) { return std::max(1, std::min(kMomMaxSplit, 512 / std::max(BH, 1))); }
+int mom_splits(int BH, int NKr) {
+    return std::max(1, std::min({kMomMaxSplit, 512 / std::max(BH, 1), (NKr + 31) / 32}));
+}
 
 // Device lambdas of the attention kernel are always inlined: a call would move the register
 // tile state through memory.
@@ -1994,7 +1997,7 @@ size_t workspace_layout(const Shape& s, char* base, Workspace* ws) {
         w.tau = reinterpret_cast<float*>(take(BH * s.NQ * 4));
         w.sigma = reinterpret_cast<float*>(take(BH * s.NQ * 4));
         w.order = reinterpret_cast<uint16_t*>(take(BH * s.NQ * 2));
-        w.mom = reinterpret_cast<double*>(take(moments_scratch_bytes(s.BH, s.d)));
+        w.mom = reinterpret_cast<double*>(take(moments_scratch_bytes(s.BH, s.NKr, s.d)));
     }
     if (s.dtype == kBF16) {
         w.vt = reinterpret_cast<_Float16*>(take(BH * d * (size_t)s.Npad * 2));
@@ -2020,22 +2023,24 @@ hipError_t launch_pool_mean(const void* x, float* mean, int dtype, int BH, int N
     return hipGetLastError();
 }
 
-size_t moments_scratch_bytes(int BH, int d) { return (size_t)BH * mom_splits(BH) * ((size_t)d * d + d) * sizeof(double); }
+size_t moments_scratch_bytes(int BH, int NKr, int d) {
+    return (size_t)BH * mom_splits(BH, NKr) * ((size_t)d * d + d) * sizeof(double);
+}
 
 hipError_t launch_moments_final(const float* kbar, float* muk, float* cov, double* scratch, int BH, int NK, int NKr,
                                 int d, hipStream_t st) {
     if (d == 128)
         moments_final_kernel<128><<<dim3(128 * 128 / 256, BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr,
-                                                                                    mom_splits(BH));
+                                                                                    mom_splits(BH, NKr));
     else
         moments_final_kernel<64><<<dim3(64 * 64 / 256, BH), dim3(256), 0, st>>>(kbar, scratch, muk, cov, NK, NKr,
-                                                                                  mom_splits(BH));
+                                                                                  mom_splits(BH, NKr));
     return hipGetLastError();
 }
 
 hipError_t launch_moments(const float* kbar, float* muk, float* cov, double* scratch, int BH, int NK, int NKr, int d,
                           hipStream_t st) {
-    const int ns = mom_splits(BH);
+    const int ns = mom_splits(BH, NKr);
     if (d == 128) moments_partial_kernel<128><<<dim3(ns, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr, ns);
     else moments_partial_kernel<64><<<dim3(ns, BH), dim3(256), 0, st>>>(kbar, scratch, NK, NKr, ns);
     hipError_t e = hipGetLastError();
