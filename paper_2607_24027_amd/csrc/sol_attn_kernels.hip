@@ -1533,8 +1533,9 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
                 if (sl < 4 * NPB) exp_pair(sl >> 2, sl & 3);
                 // Each slot is its own scheduling region: left free, the scheduler sinks the
                 // exponentials towards their PV consumers and leaves most QK^T MFMAs of the
-                // wave with no VALU work beside them (1-2% slower, measured).
-                __builtin_amdgcn_sched_barrier(0);
+                // wave with no VALU work beside them (1-2% slower, measured).  The causal
+                // kernels keep the free schedule: with the regions they ran 1-2% slower.
+                if constexpr (!CAUSAL) __builtin_amdgcn_sched_barrier(0);
             }
             bo = scores_done(t + 1, cv, n0, n1);
             mx = tile_max_l2(n0, n1, bo);
