@@ -54,6 +54,17 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) {
     return __builtin_bit_cast(uint16_t, (__bf16)x);
 }
 
+// l + p.x + p.y in f32, from the two f16 halves of p exactly as they are: two mixed-precision
+// FMAs (v_fma_mix_f32, each half times 1.0 plus the sum), the form of the row sums that issues
+// beside the PV MFMAs of the tile loop (the f16 dot product stalls the matrix pipe there).
+__device__ __forceinline__ float add_f16x2(float l, f16x2 p) {
+    asm("v_fma_mix_f32 %0, %1, 1.0, %0 op_sel_hi:[1,0,0]\n\t"
+        "v_fma_mix_f32 %0, %1, 1.0, %0 op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+        : "+v"(l)
+        : "v"(p));
+    return l;
+}
+
 // Position p of a transposed V row holds key swap23(p): bits 2 and 3 exchanged.
 __device__ __forceinline__ int swap23(int p) {
     return (p & ~12) | ((p & 8) >> 1) | ((p & 4) << 1);
@@ -1479,6 +1490,11 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
             const int cn = t + 3 < T ? code(t + 3) : 0;
             const float msub = (m_run == kNegInf ? 0.f : m_run) - bo;
             const f16x2 ones = {(_Float16)1.f, (_Float16)1.f};
+            // Row sums of the rounded P.  Non-causal kernels: the f16 dot product, right after the
+            // pair's exponentials (beside the QK^T MFMAs; in the PV slots it stalls the matrix
+            // pipe, 3-5% slower).  Causal kernels: two mixed FMAs per pair in the PV slots, 4%
+            // faster there than the dot product (their register use and schedule differ).
+            constexpr bool kRowSumInPV = CAUSAL;
             f16x8 pb[NPB];
             auto exp_pair = [&](int kk, int q) SOL_INLINE {   // elements 2q, 2q+1 of P block kk
                 const int tt = kk >> 1, r = 8 * (kk & 1) + 2 * q;
@@ -1487,7 +1503,7 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
                 const float p0 = __builtin_amdgcn_exp2f(fmaf(x0, cl, -msub));
                 const float p1 = __builtin_amdgcn_exp2f(fmaf(x1, cl, -msub));
                 const f16x2 pp = {(_Float16)p0, (_Float16)p1};
-                l_run[kk] = __builtin_amdgcn_fdot2(pp, ones, l_run[kk], false);
+                if constexpr (!kRowSumInPV) l_run[kk] = __builtin_amdgcn_fdot2(pp, ones, l_run[kk], false);
                 pb[kk][2 * q] = pp[0];
                 pb[kk][2 * q + 1] = pp[1];
             };
@@ -1531,11 +1547,16 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
                     o[id & 3] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, pb[id >> 2], o[id & 3], 0, 0, 0);
                 }
                 if (sl < 4 * NPB) exp_pair(sl >> 2, sl & 3);
+                if constexpr (kRowSumInPV) {
+                    if (sl >= NQK && sl - NQK < 4 * NPB) {   // pair sl - NQK, while its P block is read
+                        const int kk = (sl - NQK) >> 2, q = (sl - NQK) & 3;
+                        l_run[kk] = add_f16x2(l_run[kk], f16x2{pb[kk][2 * q], pb[kk][2 * q + 1]});
+                    }
+                }
                 // Each slot is its own scheduling region: left free, the scheduler sinks the
                 // exponentials towards their PV consumers and leaves most QK^T MFMAs of the
-                // wave with no VALU work beside them (1-2% slower, measured).  The causal
-                // kernels keep the free schedule: with the regions they ran 1-2% slower.
-                if constexpr (!CAUSAL) __builtin_amdgcn_sched_barrier(0);
+                // wave with no VALU work beside them (1-2% slower, measured).
+                __builtin_amdgcn_sched_barrier(0);
             }
             bo = scores_done(t + 1, cv, n0, n1);
             mx = tile_max_l2(n0, n1, bo);
