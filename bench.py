@@ -183,6 +183,21 @@ def measure(w, kept, qd, kd, vd, steps, warmup, modes=("sparse", "sparse_no_corr
             "times": t}
 
 
+def dense_block_q128(w, qd, kd, vd, steps, warmup, sparse_times):
+    """Dense mode of a shape whose routing uses 64-row query blocks, timed again with 128-row blocks.
+    Dense attention does not depend on the block size, and the 128-row kernel is the library's
+    fastest dense form, so this is the strictest dense reference for that shape."""
+    import torch
+    from paper_2607_24027_amd import binding
+    out = torch.empty_like(qd)
+    log(f"timing {w.name} dense with 128-row blocks")
+    d = time_steps(lambda: binding.forward(qd, kd, vd, 128, w.block_k, float("-inf"), "dense", 0, out=out),
+                   steps, warmup)
+    sp = sparse_times
+    return {"kernel_ms": round(d["kernel"], 4), "step_ms": round(d["mean"], 4),
+            "speedup_kernel": round(d["kernel"] / sp["kernel"], 4), "speedup_step": round(d["mean"] / sp["mean"], 4)}
+
+
 def summary(m, dense, w):
     """Compact record of a measured point against a dense-mode timing of the same shape."""
     r4 = lambda x: round(x, 4)
@@ -251,6 +266,8 @@ def main():
                                                   / MFMA_BF16_PEAK_TFLOPS, 4),
                     "shape": f"B={w.B} H={w.H} N={w.N} d={w.d} blocks {w.block_q}x{w.block_k}"
                              + (f", {w.text_tokens} forced text tokens" if w.text_tokens else "")})
+        if w.block_q != 128:
+            rec["dense_block_q128"] = dense_block_q128(w, qd, kd, vd, args.steps, args.warmup, mo["times"]["sparse"])
         print(json.dumps(rec), flush=True)
         return
 
@@ -305,6 +322,8 @@ def main():
                      "flop_per_launch": exact_flop + approx_flop, "exact_flop": exact_flop,
                      "correction_flop": approx_flop},
     }
+    if w.block_q != 128:
+        res["dense_block_q128"] = dense_block_q128(w, qd, kd, vd, args.steps, args.warmup, sp)
     if not args.no_extras and w.name == "video720p" and args.kept is None:
         # The other kept fractions of the 720p sweep (same inputs, same dense timing) ...
         xs, xw = max(3, args.steps // 4), 2
