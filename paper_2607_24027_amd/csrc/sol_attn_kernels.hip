@@ -1547,6 +1547,15 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
                     o[id & 3] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av, pb[id >> 2], o[id & 3], 0, 0, 0);
                 }
                 if (sl < 4 * NPB) exp_pair(sl >> 2, sl & 3);
+                // row max of tile t+1 in the second-last slot (0.2-0.8% faster than after the last;
+                // the causal kernels take it after the loop: their masked form inside the
+                // unrolled loop multiplies the code)
+                if constexpr (!CAUSAL) {
+                    if (sl == NSLOT - 2) {
+                        bo = scores_done(t + 1, cv, n0, n1);
+                        mx = tile_max_l2(n0, n1, bo);
+                    }
+                }
                 if constexpr (kRowSumInPV) {
                     if (sl >= NQK && sl - NQK < 4 * NPB) {   // pair sl - NQK, while its P block is read
                         const int kk = (sl - NQK) >> 2, q = (sl - NQK) & 3;
@@ -1558,8 +1567,10 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
                 // wave with no VALU work beside them (1-2% slower, measured).
                 __builtin_amdgcn_sched_barrier(0);
             }
-            bo = scores_done(t + 1, cv, n0, n1);
-            mx = tile_max_l2(n0, n1, bo);
+            if constexpr (CAUSAL) {
+                bo = scores_done(t + 1, cv, n0, n1);
+                mx = tile_max_l2(n0, n1, bo);
+            }
             __builtin_amdgcn_s_waitcnt(0);
             __syncthreads();
             s0 = n0;
