@@ -1535,6 +1535,11 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
             int uk = 0, uv = 0;   // operands consumed so far
 #pragma unroll
             for (int sl = 0; sl < NSLOT; ++sl) {
+                // Wave priority: highest in the QK^T half (the exponentials), lower in the PV half,
+                // lowest outside the tile loops (routing, epilogue), which the other workgroup on the
+                // CU can then overlap: 1-2.4% faster in the sparse modes, dense within noise.
+                if (sl == 0) __builtin_amdgcn_s_setprio(2);
+                if (sl == NQK) __builtin_amdgcn_s_setprio(1);
                 prefetch(sl + 2);
                 const int id = index(sl);
                 if (kind(sl) == 0) {
@@ -1608,7 +1613,9 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
 #pragma unroll
             for (int e = 0; e < 8; ++e) qh[ks][e] = (_Float16)(float)qv[e];
         }
+        __builtin_amdgcn_s_setprio(1);
         pipeline(APX_T{}, qh, napx, [&](int t) SOL_INLINE { return t; });
+        __builtin_amdgcn_s_setprio(0);
         __syncthreads();   // the stages are refilled below while the last V tile may still be read
     }
     const int T = ntiles;
@@ -1617,7 +1624,9 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
 #pragma unroll
         for (int ks = 0; ks < NKS; ++ks)
             qf[ks] = qrow < a.N ? *reinterpret_cast<const bf16x8*>(qrow_p + 16 * ks) : bf16x8{};
+        __builtin_amdgcn_s_setprio(1);
         pipeline(EXACT_T{}, qf, T, [&](int t) SOL_INLINE { return tile_code(t); });
+        __builtin_amdgcn_s_setprio(0);
     }
 
     // ---- epilogue: O = O^T / l, bf16
