@@ -64,6 +64,10 @@ def fwd(*, B=1, H=2, N=1000, d=128, bq=128, bk=64, tau=0.5, mode=1, dtype=0, kee
     (dict(bk=32), sb.SOL_ERR_UNSUPPORTED),
     (dict(bq=256), sb.SOL_ERR_UNSUPPORTED),
     (dict(N=64 * 60000), sb.SOL_ERR_UNSUPPORTED),
+    # the routing state of a block lives in LDS: at d = 128 the last supported length is 1,478,656
+    # tokens (23,104 key blocks), at d = 64 1,971,200 (30,800 key blocks)
+    (dict(N=1478656 + 64), sb.SOL_ERR_UNSUPPORTED),
+    (dict(N=1971200 + 64, d=64), sb.SOL_ERR_UNSUPPORTED),
 ])
 def test_forward_validation(kwargs, code):
     assert fwd(**kwargs) == code
@@ -86,6 +90,8 @@ def fwdc(*, B=1, H=2, N=1000, d=128, bq=128, bk=64, tau=0.5, mode=1, dtype=0, gr
     (dict(bq=32), sb.SOL_ERR_UNSUPPORTED),
     # the per-row proxies of a causal row live in LDS: 15000 key blocks fit without a mask only
     (dict(N=64 * 15000), sb.SOL_ERR_UNSUPPORTED),
+    (dict(N=761856 + 64), sb.SOL_ERR_UNSUPPORTED),
+    (dict(N=1015808 + 64, d=64, bq=128), sb.SOL_ERR_UNSUPPORTED),
 ])
 def test_causal_forward_validation(kwargs, code):
     assert fwdc(**kwargs) == code
