@@ -16,11 +16,11 @@
  * N >= 1 with ragged last blocks (a block's statistics use only its valid
  * tokens); bf16 inputs (the hot path) and f32 inputs (a correctness-first
  * path).  The per-block routing lists live on chip, which bounds N: bf16 at
- * d = 128 up to about 1.48M tokens (760K with a causal mask), at d = 64 up to
- * about 1.97M (1.0M causal); beyond that the forward returns
- * SOL_ERR_UNSUPPORTED.  Two workgroups share a compute unit up to about 245K
- * tokens at d = 128 (126K causal) and 737K at d = 64 (380K causal); longer
- * sequences run with one and take roughly twice as long per tile.  The softmax scale is 1/sqrt(d) for the exact logits and the
+ * d = 128 up to 1,478,656 tokens (1,048,576 with a causal mask), at d = 64 up
+ * to 1,971,200 (1,015,808 causal); beyond that the forward returns
+ * SOL_ERR_UNSUPPORTED.  Two workgroups share a compute unit up to 245,760
+ * tokens at d = 128 (causal too) and 737,280 at d = 64 (524,288 causal);
+ * longer sequences run with one and take roughly twice as long per tile.  The softmax scale is 1/sqrt(d) for the exact logits and the
  * proxies alike.
  *
  * Range contract of the bf16 path (checked by nobody: outside it results are

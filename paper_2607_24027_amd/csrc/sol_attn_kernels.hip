@@ -1002,7 +1002,11 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, char* smem, const 
     uint32_t* selw = reinterpret_cast<uint32_t*>(rest + 64);
     uint16_t* list = reinterpret_cast<uint16_t*>(rest + 64 + 4 * ((a.MW + 3) & ~3));
     int* wpre = reinterpret_cast<int*>(rest + ((64 + 4 * ((a.MW + 3) & ~3) + 2 * (a.NC * kChunk + a.NK) + 15) & ~15));
-    float* prox = reinterpret_cast<float*>(wpre + ((a.MW + 3) & ~3));   // after the word prefixes
+    // The causal prologue's per-row proxies: in the tile stages, which no copy fills before the
+    // routing is done (the block loop's barrier ends every read of the previous block's tiles),
+    // when they fit there; else after the word prefixes.
+    float* prox = 4 * a.NKr <= 2 * L::STAGE ? reinterpret_cast<float*>(smem)
+                                             : reinterpret_cast<float*>(wpre + ((a.MW + 3) & ~3));
     const uint16_t* ulist = list;            // correction slots (unselected routable blocks, padded)
     const uint16_t* elist = list + a.NC * kChunk;   // exact tiles
 
@@ -2019,11 +2023,13 @@ size_t attn_lds_bytes(const Shape& s) {
     // scan scratch, selection words, lists, then (16-byte aligned) the words' prefix counts
     size_t rest = 64 + 4 * (size_t)((s.MW + 3) & ~3) + 2 * ((size_t)s.NC * kChunk + s.NK);
     rest = ((rest + 15) & ~(size_t)15) + 4 * (size_t)((s.MW + 3) & ~3);
-    if (s.causal && s.mode != kDense) rest += 4 * (size_t)s.NKr;   // proxies of a row
     if (s.dtype == kBF16) {
         const size_t stage = (size_t)kBlockK * s.d * 2 * 2;
+        // proxies of a causal row: in the tile stages when they fit (the kernel decides alike)
+        if (s.causal && s.mode != kDense && 4 * (size_t)s.NKr > 2 * stage) rest += 4 * (size_t)s.NKr;
         return 2 * stage + rest;
     }
+    if (s.causal && s.mode != kDense) rest += 4 * (size_t)s.NKr;   // proxies of a row
     return (size_t)2 * kBlockK * s.d * 4 + (size_t)s.d * s.bq * 4 + rest;
 }
 

@@ -88,9 +88,10 @@ def fwdc(*, B=1, H=2, N=1000, d=128, bq=128, bk=64, tau=0.5, mode=1, dtype=0, gr
     (dict(ptrs=[FAKE[0], None, FAKE[2], FAKE[3]]), sb.SOL_ERR_INVALID_ARG),
     (dict(d=96), sb.SOL_ERR_UNSUPPORTED),
     (dict(bq=32), sb.SOL_ERR_UNSUPPORTED),
-    # the per-row proxies of a causal row live in LDS: 15000 key blocks fit without a mask only
-    (dict(N=64 * 15000), sb.SOL_ERR_UNSUPPORTED),
-    (dict(N=761856 + 64), sb.SOL_ERR_UNSUPPORTED),
+    # a causal row's proxies live in the tile stages while they fit there (16384 key blocks at
+    # d = 128), and past that beside the lists, which no longer fit: 16385 key blocks fit without
+    # a mask only
+    (dict(N=64 * 16385), sb.SOL_ERR_UNSUPPORTED),
     (dict(N=1015808 + 64, d=64, bq=128), sb.SOL_ERR_UNSUPPORTED),
 ])
 def test_causal_forward_validation(kwargs, code):
@@ -101,7 +102,7 @@ def test_causal_forward_validation(kwargs, code):
 def test_causal_sizes_accepted_without_mask():
     # same size as the rejected causal case passes validation without the mask (fails only
     # later, at the fake pointers, which validation never reaches here: use the workspace query)
-    assert sb.workspace_bytes(1, 2, 64 * 15000, 128, 128, 64, "sparse") > 0
+    assert sb.workspace_bytes(1, 2, 64 * 16385, 128, 128, 64, "sparse") > 0
 
 
 def test_other_entry_points_validate():
