@@ -86,6 +86,56 @@ def test_causal_parity_small(dev, name, mode, beta):
     assert_output_close(to_np(out), ref["out"], w.dtype, f"causal {name}/{mode}/{beta}")
 
 
+def random_causal_case(seed):
+    """A seeded random causal configuration: token grid, block sizes, dtype, granule, cutoff, mode."""
+    rng = np.random.default_rng(2000 + seed)
+    d = int(rng.choice([64, 128]))
+    bq = int(rng.choice([64, 128]))
+    dtype = "f32" if rng.random() < 0.2 else "bf16"
+    n_img = int(rng.integers(1, 6000))
+    shape = int(rng.integers(1, 4))                       # 1D, 2D or 3D token grid
+    if shape == 1:
+        grid = (n_img,)
+    elif shape == 2:
+        a = int(rng.integers(1, 80))
+        grid = (a, max(1, n_img // a))
+    else:
+        a, b = int(rng.integers(1, 12)), int(rng.integers(1, 30))
+        grid = (a, b, max(1, n_img // (a * b)))
+    n = int(np.prod(grid))
+    r = rng.random()
+    g = 1 if r < 0.3 else (n if r < 0.4 else int(rng.integers(1, n + 1)))   # token, bidirectional, any
+    B, H = int(rng.integers(1, 3)), int(rng.integers(1, 4))
+    r = rng.random()
+    beta = -INF if r < 0.1 else (INF if r < 0.2 else float(np.round(rng.uniform(-1.0, 2.0), 3)))
+    mode = str(rng.choice(["dense", "sparse", "sparse_no_correction"]))
+    return grid, d, bq, dtype, g, B, H, beta, mode
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_causal_parity_random_shapes(dev, seed):
+    # Seeded random causal configurations (any token count, ragged tails, 1D/2D/3D grids, granules
+    # from one token to the whole sequence, both dtypes and block heights, cutoffs from -inf to
+    # +inf), element by element.
+    grid, d, bq, dtype, g, B, H, beta, mode = random_causal_case(seed)
+    w = small_workload(f"crand{seed}", grid, d, bq, dtype=dtype, H=H, B=B, seed=90 + seed)
+    print(f"[causal] random {seed}: grid={grid} N={w.N} d={d} bq={bq} {dtype} G={g} B={B} H={H} beta={beta} "
+          f"{mode}", flush=True)
+    q, k, v = synth.make_qkv(w)
+    out, gmask, counts = run_causal(dev, w, g, q, k, v, beta, mode)
+    assert bool(torch.isfinite(out).all())
+    qn, kn, vn = to_np(q), to_np(k), to_np(v)
+    ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, causal_granule=g)
+    if mode != "dense":
+        flips = assert_mask_matches(gmask, ref["mask"], ref["s_hat"], ref["tau"])
+        if flips:
+            ref = ora.forward(qn, kn, vn, w.block_q, 64, beta, mode, causal_granule=g, mask=gmask)
+        assert np.array_equal(counts, gmask.sum(axis=(2, 3)))
+    else:
+        assert np.all(counts == routable_pairs(w, g))
+    assert_output_close(to_np(out), ref["out"], w.dtype, f"causal random {seed}")
+
+
 def test_causal_full_selection_is_bitwise_dense(dev):
     w, g, (q, k, v) = inputs("bf16_d128_q128_token")
     dense, _, _ = run_causal(dev, w, g, q, k, v, 0.0, "dense")
